@@ -1,0 +1,319 @@
+#!/usr/bin/env python3
+"""Throughput of the REFLEX variable-K MoE layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one full pass of the layer (router -> counts -> TopK -> permutation ->
+SwiGLU experts -> combine) over the workload's tokens, through
+``reflex_moe_forward_timed``; for the 16-layer stack it is all 16 layers, with
+counts computed once and shared by every layer.  Inputs and weights are resident
+in device memory before timing starts.  HIP events recorded by the library at
+every stage boundary give per-stage times; the stage that dominates gets a
+roofline figure from its algorithmic bytes (or FLOPs) per launch.  The
+fixed-count path (k_i = K_base, default token-choice routing) is timed alongside.
+The CPU oracle is timed on a bounded sample of the same workload as a reported
+baseline.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s + TFLOP/s (alloc. expert FLOPs) as % bf16 MFMA peak, var-K"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+DEFAULT_WORKLOAD = "lladamoe_t1024_e64"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch has loaded (same soname)."""
+
+    def __init__(self):
+        import torch  # noqa: F401  (loads the runtime first)
+        h = ctypes.CDLL("libamdhip64.so.7")
+        vp = ctypes.c_void_p
+        h.hipEventCreate.argtypes = [ctypes.POINTER(vp)]
+        h.hipEventDestroy.argtypes = [vp]
+        h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+        self.h = h
+        self.events = []
+
+    def create(self):
+        e = ctypes.c_void_p()
+        rc = self.h.hipEventCreate(ctypes.byref(e))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        self.events.append(e.value)
+        return e.value
+
+    def ms(self, a, b) -> float:
+        out = ctypes.c_float()
+        rc = self.h.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(out.value)
+
+    def close(self):
+        for e in self.events:
+            self.h.hipEventDestroy(e)
+        self.events = []
+
+
+def expert_counts(lay, h, state, torch):
+    """Per-expert pair counts of the counts the layer just used, through the library's
+    own TopK and permutation entry points (outside the timed region)."""
+    from paper_2608_01784_amd import _lib
+    T, E = lay.T, lay.w.E
+    cap = T * lay.kcap
+    off = torch.empty(T + 1, dtype=torch.int32, device="cuda")
+    ex = torch.empty(max(cap, 1), dtype=torch.int32, device="cuda")
+    wt = torch.empty(max(cap, 1), dtype=torch.float32, device="cuda")
+    _lib.reflex_topk_variable(lay.logits, lay.k, lay.kcap, lay.norm_topk, off, ex, wt)
+    eo = torch.empty(E + 1, dtype=torch.int32, device="cuda")
+    st = torch.empty(max(cap, 1), dtype=torch.int32, device="cuda")
+    p2s = torch.empty(max(cap, 1), dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(_lib.reflex_permute_workspace_size(cap, E), 256), dtype=torch.uint8,
+                     device="cuda")
+    _lib.reflex_permute(off, ex, off[T:T + 1], E, eo, st, p2s, ws)
+    torch.cuda.synchronize()
+    import numpy as np
+    return np.diff(eo.cpu().numpy())
+
+
+def stage_roofline(stage, ms, d, f, P, touched, T, E):
+    """Algorithmic work of one launch of a stage: bytes each operand must move once,
+    FLOPs of its contraction; bound = the larger of the two times at peak."""
+    if stage == "gemm_up":
+        flops = 4 * d * f * P
+        nbytes = touched * 2 * f * d * 2 + P * d * 2 + P * f * 2
+    elif stage == "gemm_down":
+        flops = 2 * d * f * P
+        nbytes = touched * d * f * 2 + P * f * 2 + P * d * 2
+    elif stage == "router":
+        flops = 2 * T * E * d
+        nbytes = T * d * 2 + E * d * 4 + T * E * 4
+    elif stage == "combine":
+        flops = 0
+        nbytes = P * d * 2 + P * 8 + (T + 1) * 4 + T * d * 2
+    elif stage == "topk":
+        flops = 0
+        nbytes = T * E * 4 + T * 4 + (T + 1) * 4 + P * 8
+    elif stage == "permute":
+        flops = 0
+        nbytes = P * 4 * 4 + (T + 1) * 4
+    else:
+        return None
+    t_mem = nbytes / (PEAK_HBM_GBS * 1e9)
+    t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
+    if flops and t_mfma > t_mem:
+        ach = flops / (ms * 1e-3) / 1e12
+        return {"kernel": stage, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "algorithmic_flops": int(flops), "algorithmic_bytes": int(nbytes), "ms": round(ms, 5)}
+    ach = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": stage, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+            "algorithmic_bytes": int(nbytes), "algorithmic_flops": int(flops), "ms": round(ms, 5)}
+
+
+def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: HipEvents):
+    """Time `steps` steps of the layer (or layer stack); returns timings and the layer
+    objects used."""
+    from paper_2608_01784_amd import _lib
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer
+    L = w.n_layers
+    lays = [MoELayer(w.T, w.d, ExpertWeights(**dws[l]), w.params, uniform_k=uniform_k) for l in range(L)]
+    res = residuals
+    hbuf = [h0, torch.empty_like(h0), torch.empty_like(h0)]
+    evs = [[[ev.create() for _ in range(_lib.N_STAGE_EVENTS)] for _ in range(L)]
+           for _ in range(steps)]
+
+    def step(events=None):
+        h = hbuf[0]
+        k_in = None
+        for l in range(L):
+            lay = lays[l]
+            out = hbuf[1 + (l & 1)] if L > 1 else None
+            args = lay.args(h, state if k_in is None else None, k_in=k_in,
+                            residual_a=h if L > 1 else None,
+                            residual_b=res[l] if (L > 1 and res is not None) else None, out=out)
+            if events is None:
+                _lib.reflex_moe_forward(args, lay.ws)
+            else:
+                _lib.reflex_moe_forward_timed(args, lay.ws, events[l])
+            if L > 1:
+                k_in = lays[0].k
+                h = out
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stage_ms = {}
+    for i, name in enumerate(_lib.STAGES):
+        stage_ms[name] = sum(ev.ms(evs[s][l][i], evs[s][l][i + 1]) for s in range(steps)
+                             for l in range(L)) / (steps * L)
+    gpu_step_ms = sum(ev.ms(evs[s][0][0], evs[s][L - 1][_lib.N_STAGE_EVENTS - 1])
+                      for s in range(steps)) / steps
+    return {"wall_ms": (t1 - t0) * 1e3 / steps, "gpu_ms": gpu_step_ms, "stage_ms": stage_ms,
+            "layers": lays}
+
+
+def cpu_baseline(w, host, seconds):
+    """Time the oracle (as it is) on a bounded sample of the workload."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    wg, wu, wd = host["w_gate"], host["w_up"], host["w_down"]
+    wof = lambda e: (wg[e], wu[e], wd[e])  # noqa: E731
+    n_sample = w.T if w.T <= 4096 else 1024
+    toks = None if n_sample == w.T else np.sort(np.random.default_rng(0).choice(w.T, n_sample, replace=False))
+    t_route = t_exp = 0.0
+    reps = 0
+    t_start = time.perf_counter()
+    while True:
+        a = time.perf_counter()
+        bud = oracle.assign_budget(w.block_idx, w.masked, w.hist_len, w.conf_prev1, w.conf_prev2,
+                                   w.seq_offsets, w.active_block, w.params)
+        r = oracle.router_scores(w.h, host["w_router"], w.router_bias)
+        route = oracle.topk_route(r, bud.k, w.norm_topk)
+        oracle.pair_permutation(route.token, route.expert, w.E)
+        b = time.perf_counter()
+        oracle.moe_layer(w.h, route, wof, w.E, shared=host["shared"], tokens=toks)
+        c = time.perf_counter()
+        t_route += b - a
+        t_exp += c - b
+        reps += 1
+        if c - t_start >= seconds:
+            break
+    per_layer = (t_route + t_exp * (w.T / n_sample)) / reps
+    sample = (f"{reps} full oracle layer(s) of {w.name}" if toks is None else
+              f"{reps} rep(s): routing on all {w.T} tokens, experts+combine on {n_sample} sampled "
+              f"tokens, scaled to {w.T}")
+    return {"value": round(w.T / per_layer, 2), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle", "sample": sample + f"; {w.n_layers} layer(s) per step counted",
+            "seconds": round(t_route + t_exp, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-uniform", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(no collectives, no sharding); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_01784_amd import _lib
+    from paper_2608_01784_amd.layer import TokenState
+    from synth import make_workload
+    from synth.device import state_tensors, to_device
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    _lib.lib()
+    log(f"generating {a.workload} (seed {a.seed})")
+    w = make_workload(a.workload, seed=a.seed)
+    hosts, dws = [], []
+    for l in range(w.n_layers):
+        host = {"w_gate": w.w_gate(l), "w_up": w.w_up(l), "w_down": w.w_down(l),
+                "w_router": w.w_router(l), "shared": w.shared_weights(l)}
+        dv = {k: to_device(host[k]) for k in ("w_gate", "w_up", "w_down", "w_router")}
+        dv["router_bias"] = None if w.router_bias is None else to_device(w.router_bias)
+        if host["shared"] is not None:
+            dv["ws_gate"], dv["ws_up"], dv["ws_down"] = (to_device(x) for x in host["shared"])
+        dws.append(dv)
+        hosts.append(host if l == 0 else None)
+        if w.n_layers > 1:
+            log(f"layer {l} weights resident")
+    residuals = [to_device(w.residual(l)) for l in range(w.n_layers)] if w.n_layers > 1 else None
+    h0 = to_device(w.h)
+    state = TokenState(**state_tensors(w))
+    torch.cuda.synchronize()
+
+    ev = HipEvents()
+    log(f"timing variable-K path: {a.warmup} warmup + {a.steps} steps")
+    var = run_path(torch, w, dws, residuals, h0, state, 0, a.steps, a.warmup, ev)
+    lay0 = var["layers"][0]
+    P = int(lay0.pairs.item())
+    counts = expert_counts(lay0, h0, state, torch)
+    touched = int((counts > 0).sum())
+    uni = None
+    if not a.no_uniform:
+        log("timing fixed-count path (k = K_base)")
+        uni = run_path(torch, w, dws, residuals, h0, state, w.params.k_base, a.steps, a.warmup, ev)
+    ev.close()
+
+    T, d, f, E, L = w.T, w.d, w.f, w.E, w.n_layers
+    step_ms = var["wall_ms"]
+    tokens_per_s = T / (step_ms * 1e-3)
+    alloc_flops = 6 * d * f * P * L                # Eq. (10) per step
+    alloc_tflops = alloc_flops / (step_ms * 1e-3) / 1e12
+    stages = var["stage_ms"]
+    dom = max(("gemm_up", "gemm_down", "router", "combine", "topk", "permute"), key=lambda s: stages[s])
+    roof = stage_roofline(dom, stages[dom], d, f, P, touched, T, E)
+    out = {
+        "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "tokens": T, "hidden": d, "experts": E, "expert_ffn": f,
+                   "shared_ffn": w.f_shared, "layers": L, "k_base": w.params.k_base,
+                   "k_range": [w.params.k_min, w.params.k_max], "path": "variable-K (REFLEX)"},
+        "alloc_tflops": round(alloc_tflops, 2),
+        "pct_bf16_peak": round(100 * alloc_tflops / PEAK_BF16_TFLOPS, 2),
+        "pairs_per_layer": P, "avg_k": round(P / T, 4), "experts_touched": touched,
+        "max_expert_rows": int(counts.max()), "gpu_ms_per_step": round(var["gpu_ms"], 4),
+        "stage_ms": {k: round(v, 5) for k, v in stages.items()},
+        "roofline": roof,
+        "roofline_all": {s: stage_roofline(s, stages[s], d, f, P, touched, T, E)
+                         for s in ("gemm_up", "gemm_down", "router", "topk", "permute", "combine")},
+    }
+    if uni is not None:
+        lu = uni["layers"][0]
+        Pu = int(lu.pairs.item())
+        u_ms = uni["wall_ms"]
+        out["uniform"] = {"k": w.params.k_base, "ms_per_step": round(u_ms, 4),
+                          "tokens_per_s": round(T / (u_ms * 1e-3), 1), "pairs_per_layer": Pu,
+                          "alloc_tflops": round(6 * d * f * Pu * L / (u_ms * 1e-3) / 1e12, 2),
+                          "stage_ms": {k: round(v, 5) for k, v in uni["stage_ms"].items()}}
+        out["var_over_uniform"] = {"pairs": round(P / Pu, 4), "time": round(step_ms / u_ms, 4)}
+    if not a.no_cpu_baseline:
+        log(f"timing the CPU oracle (~{a.cpu_seconds:.0f} s)")
+        out["cpu_baseline"] = cpu_baseline(w, hosts[0], a.cpu_seconds)
+        if L > 1:
+            out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"] / L, 2)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

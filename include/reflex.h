@@ -1,0 +1,272 @@
+/*
+ * reflex.h - C ABI of the REFLEX variable-K MoE layer for MI355X (gfx950).
+ *
+ * The layer is the MoE feed-forward block of a diffusion language model's
+ * denoising forward in which each token i gets its own expert count k_i
+ * (Section 3.2, Eq. (2)), chosen per forward by Refinement-Role Budgeting
+ * (Section 4.2, Eq. (5)) and Frontier-Guided Expert Reallocation with the
+ * Frontier-Progress Score (Section 4.3, Eqs. (6)-(9)), subject to the count
+ * bounds of Eq. (3).
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or retains them.  Struct arguments
+ *    (reflex_alloc_params, reflex_moe_args) are HOST pointers, read during the
+ *    call only.
+ *  - bf16 data is passed as uint16_t bit patterns.  Matrices are row-major and
+ *    dense (leading dimension = row length).
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Work is
+ *    enqueued asynchronously; nothing is read back to the host and no call
+ *    synchronises.  Calls are stateless and may be made from several threads.
+ *  - Arguments are validated on the host before anything is launched; on error
+ *    nothing is launched and a negative status is returned.  No C++ exception
+ *    crosses the ABI.
+ *  - T = 0 (no tokens) is valid and enqueues nothing.
+ *  - Every device pointer must be 16-byte aligned (REFLEX_ERR_SHAPE otherwise);
+ *    the kernels move data in 16-byte vectors.
+ *  - Content preconditions that cannot be checked without reading device memory
+ *    (seq_offsets non-decreasing from 0 to T, block_idx >= 0, hist_len in
+ *    {0,1,2}, finite logits, expert_offsets consistent with the pair count) are
+ *    the caller's.  Kernels never index outside the buffers whose sizes the
+ *    arguments state, whatever those contents are: counts are clamped to
+ *    [0, k_max] before they size anything.
+ */
+#ifndef REFLEX_H
+#define REFLEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------------ */
+#define REFLEX_OK                 0
+#define REFLEX_ERR_NULL         (-1)  /* a required pointer is NULL                        */
+#define REFLEX_ERR_SHAPE        (-2)  /* a size is out of range or not a supported multiple */
+#define REFLEX_ERR_PARAM        (-3)  /* a hyper-parameter is out of range or not finite    */
+#define REFLEX_ERR_WORKSPACE    (-4)  /* workspace or pair capacity too small               */
+#define REFLEX_ERR_LAUNCH       (-5)  /* the HIP runtime reported a launch error            */
+#define REFLEX_ERR_UNSUPPORTED  (-6)  /* a valid request this build does not implement      */
+
+/* ---- limits ------------------------------------------------------------------ */
+#define REFLEX_MAX_EXPERTS  256       /* E <= 256                                        */
+#define REFLEX_MAX_K        32        /* k_max <= min(E, 32)                             */
+#define REFLEX_D_MULTIPLE   128       /* hidden size d must be a multiple of this        */
+#define REFLEX_F_MULTIPLE   64        /* expert widths f, f_shared must be multiples     */
+#define REFLEX_MAX_DIM      16384     /* d, f, f_shared <= this                          */
+#define REFLEX_MAX_TOKENS   (1 << 24) /* T <= this                                       */
+
+/* Ranking key of the active-block reallocation (Section 4.3; Appendix C). */
+#define REFLEX_SIGNAL_FPS          0  /* S = F * P, Eq. (8)                    */
+#define REFLEX_SIGNAL_FRONTIER     1  /* F alone, Eq. (6)                      */
+#define REFLEX_SIGNAL_PROGRESS     2  /* P alone, Eq. (7)                      */
+#define REFLEX_SIGNAL_CONFIDENCE   3  /* lagged confidence c^{t-1}             */
+#define REFLEX_SIGNAL_UNCERTAINTY  4  /* 1 - c^{t-1}                           */
+
+/*
+ * Allocation hyper-parameters (Eqs. (3), (5)-(9); defaults in Section 5.1:
+ * k_base 8, delta_role 4, delta_cur 2, q 0.25, theta 0.9, w_cf 0.30 or 0.25,
+ * v_ref 0.01, tau 0.05).  Real values are float32 and are widened exactly to
+ * fp64 inside the kernels.
+ * Valid: 0 <= k_min <= k_max <= REFLEX_MAX_K; k_base, delta_role, delta_cur >= 0;
+ * 0 < q <= 0.5; tau > 0; w_cf > 0; theta, v_ref finite; signal in 0..4.
+ */
+typedef struct {
+  int32_t k_base;      /* K_base: nominal count (Eq. (5))                            */
+  int32_t delta_role;  /* delta_role: role offset (Eq. (5)); K_cur = k_base+delta_role */
+  int32_t delta_cur;   /* delta_cur: reallocation offset (Eq. (9))                  */
+  int32_t k_min;       /* K_min: lower count bound (Eq. (3)), applied as a clamp     */
+  int32_t k_max;       /* K_max: upper count bound (Eq. (3)), applied as a clamp     */
+  float   q;           /* outer-group fraction; groups have floor(q*m) members      */
+  float   theta;       /* commitment threshold theta                                */
+  float   w_cf;        /* commitment-frontier width w_cf                            */
+  float   v_ref;       /* velocity reference v_ref                                  */
+  float   tau;         /* gate temperature tau                                      */
+  int32_t signal;      /* REFLEX_SIGNAL_*                                           */
+} reflex_alloc_params;
+
+/* ---- introspection ---------------------------------------------------------- */
+int         reflex_version(void);               /* 100 * major + minor                */
+const char* reflex_status_string(int status);   /* static string, never NULL          */
+size_t      reflex_sizeof_alloc_params(void);   /* sizeof(reflex_alloc_params)        */
+size_t      reflex_sizeof_moe_args(void);       /* sizeof(reflex_moe_args)            */
+
+/* ---- workspace sizes ----------------------------------------------------------
+ * Bytes of device scratch the entry points below need; 0 on invalid sizes.
+ * reflex_workspace_size covers reflex_moe_forward and is also large enough for
+ * reflex_permute and reflex_grouped_swiglu with pair_capacity = T * k_max. */
+size_t reflex_workspace_size(int T, int E, int d, int f, int f_shared, int k_max);
+size_t reflex_permute_workspace_size(int pair_capacity, int E);
+size_t reflex_swiglu_workspace_size(int pair_capacity, int E, int f);
+
+/*
+ * Router scores r_{i,e} = sum_k h[i,k] * w_router[e,k] (+ bias[e])  (Section 3.2).
+ *  h        [T, d]  bf16   token representations
+ *  w_router [E, d]  fp32   router weight (nn.Linear layout)
+ *  bias     [E]     fp32   optional per-expert offset, NULL for none
+ *  logits   [T, E]  fp32   output; products of the bf16 input and the fp32 weight
+ *                          are accumulated in fp32 (max row error ~1e-6 relative)
+ * Errors: NULL h/w_router/logits; T, d or E out of range (d % 128, 1 <= E <= 256).
+ */
+int reflex_router_logits(const uint16_t* h, const float* w_router, const float* bias,
+                         float* logits, int T, int d, int E, void* stream);
+
+/*
+ * Per-token expert counts for one denoising forward (the allocator Pi of Eq. (3)).
+ * For every sequence s (tokens seq_offsets[s] .. seq_offsets[s+1]-1, active block
+ * active_block[s]):
+ *   1. RRB prior k_i = H(|b(i) - a_s|)  (Eq. (5)); prompt tokens have b = 0.
+ *   2. J = masked tokens of the active block (Section 3.1).  Tokens of J with
+ *      hist_len >= 1 are ranked by the key `params->signal` selects, in fp64,
+ *      descending, ties to the lower token index; the first floor(q*m) get
+ *      K_cur + delta_cur, the last floor(q*m) get K_cur - delta_cur, the rest
+ *      K_cur (Eq. (9)).  Tokens of J with no history keep K_cur.
+ *      Forecast (Section 4.3): hist 2: v = c1 - c2 clipped to +-w_cf/2,
+ *      c_hat = clip(c1 + v, 0, 1); hist 1: v = 0, c_hat = c1, P = 1.
+ *   3. Every count is clamped to [k_min, k_max].
+ *  block_idx   [T] int32   b(i) >= 0
+ *  masked      [T] uint8   nonzero = position still [MASK]
+ *  hist_len    [T] int8    number of confidence observations available (0..2)
+ *  conf_prev1  [T] fp32    c^{t-1};  conf_prev2 [T] fp32  c^{t-2}
+ *  seq_offsets [B+1] int32 token ranges, non-decreasing, 0 .. T
+ *  active_block[B] int32   a_s >= 1
+ *  params      host pointer
+ *  k_out       [T] int32   output counts
+ *  pairs_out   [1] int32   output sum_i k_i
+ *  fps_out     [T] fp64    optional: the ranking key of every ranked token, NaN
+ *                          for tokens that are not ranked; NULL to skip
+ * Errors: NULL required pointers; T > 0 with B < 1; invalid params.
+ */
+int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
+                         const float* conf_prev1, const float* conf_prev2,
+                         const int32_t* seq_offsets, const int32_t* active_block, int B, int T,
+                         const reflex_alloc_params* params, int32_t* k_out, int32_t* pairs_out,
+                         double* fps_out, void* stream);
+
+/*
+ * Variable-count TopK and routing weights (Section 3.2, Eq. (2)).
+ * Token i keeps its min(max(k[i],0), k_max) best experts in the order (logit
+ * descending, expert index ascending; -0.0 == +0.0).  Pairs are written
+ * token-major, in rank order, at pair_offsets[i] ... pair_offsets[i+1]-1.
+ *  logits       [T, E] fp32
+ *  k            [T]    int32   counts (clamped as above)
+ *  norm_topk    1: alpha = softmax over the selected experts (sums to 1);
+ *               0: alpha = the full softmax probability over all E experts
+ *  pair_offsets [T+1]  int32   output exclusive prefix sum of the counts
+ *  pair_expert  [pair_capacity] int32  output expert of each pair
+ *  pair_weight  [pair_capacity] fp32   output alpha of each pair
+ *  pair_capacity must be >= T * k_max (REFLEX_ERR_WORKSPACE otherwise).
+ * Errors: NULL pointers; k_max < 0 or > min(E, 32); norm_topk not 0/1.
+ */
+int reflex_topk_variable(const float* logits, const int32_t* k, int T, int E, int k_max,
+                         int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
+                         float* pair_weight, int32_t pair_capacity, void* stream);
+
+/*
+ * Group the P expert-token pairs by expert: a stable counting sort of the
+ * token-major pair list by expert, so rows are ordered by (expert, token).
+ *  pair_offsets [T+1] int32, pair_expert [P] int32   from reflex_topk_variable
+ *  pairs        [1]   int32  device P (clamped to pair_capacity)
+ *  expert_offsets [E+1] int32  output: rows of expert e are
+ *                              expert_offsets[e] .. expert_offsets[e+1]-1
+ *  sorted_token [pair_capacity] int32  output: token of each expert-sorted row
+ *  pair_to_sorted [pair_capacity] int32 output: expert-sorted row of each pair
+ *  ws, ws_bytes  scratch of >= reflex_permute_workspace_size(pair_capacity, E)
+ * Errors: NULL pointers; E out of range; workspace too small.
+ */
+int reflex_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
+                   int T, int E, int32_t pair_capacity, int32_t* expert_offsets,
+                   int32_t* sorted_token, int32_t* pair_to_sorted, void* ws, size_t ws_bytes,
+                   void* stream);
+
+/*
+ * SwiGLU experts on expert-sorted rows (the expert E_e of Eq. (2); two input and
+ * one output projection as counted in Appendix A, Eq. (10)):
+ *   for each row j of expert e, x = h[sorted_token[j]],
+ *   y_sorted[j] = W_down[e] (SiLU(W_gate[e] x) * (W_up[e] x)).
+ * Both projections run on bf16 MFMA with fp32 accumulation; the activation
+ * SiLU(g)*u is rounded to bf16 once, y once.
+ *  h        [T, d] bf16;  w_gate, w_up [E, f, d] bf16;  w_down [E, d, f] bf16
+ *  y_sorted [pair_capacity, d] bf16 output (rows >= expert_offsets[E] untouched)
+ *  ws       scratch of >= reflex_swiglu_workspace_size(pair_capacity, E, f)
+ * Errors: NULL pointers; d % 128 or f % 64 nonzero; workspace too small.
+ */
+int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
+                          const int32_t* expert_offsets, const uint16_t* w_gate,
+                          const uint16_t* w_up, const uint16_t* w_down, int T, int E, int d,
+                          int f, int32_t pair_capacity, uint16_t* y_sorted, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/*
+ * Weighted combine (Eq. (2)): out[i] = sum over the pairs j of token i, in rank
+ * order, of pair_weight[j] * y_sorted[pair_to_sorted[j]], plus shared_y[i] when
+ * given; accumulated in fp32 and rounded to bf16 once.
+ *  y_sorted [pair_capacity, d] bf16; pair_offsets [T+1];
+ *  pair_to_sorted, pair_weight [pair_capacity]  (pair indices and rows are clamped
+ *                          to [0, pair_capacity) before use)
+ *  shared_y [T, d] bf16 optional (always-on shared expert, weight 1)
+ *  out      [T, d] bf16 output
+ * Errors: NULL pointers; d % 128 nonzero; pair_capacity < 0.
+ */
+int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
+                   const int32_t* pair_to_sorted, const float* pair_weight,
+                   const uint16_t* shared_y, int T, int d, int32_t pair_capacity, uint16_t* out,
+                   void* stream);
+
+/*
+ * The whole layer on one stream, no host synchronisation: router -> counts ->
+ * TopK -> permutation -> SwiGLU experts -> combine (+ shared expert, + residuals).
+ * Count source, first match wins:
+ *   k_in != NULL   reuse counts computed earlier in the same forward (the paper
+ *                  shares k_i across MoE layers, Section 3.3);
+ *   uniform_k > 0  default fixed token-choice routing, k_i = uniform_k;
+ *   otherwise      reflex_assign_budget with `params` and the token state.
+ * Pair capacity is T * kcap with kcap = uniform_k if uniform_k > 0, else params.k_max.
+ */
+typedef struct {
+  int32_t T, d, E, f;
+  int32_t f_shared;        /* width of the always-on shared expert, 0 = none           */
+  int32_t norm_topk;       /* as in reflex_topk_variable                               */
+  int32_t uniform_k;       /* > 0: fixed count for every token                         */
+  int32_t B;               /* number of sequences (budget path)                         */
+  const uint16_t *h;                         /* [T, d]                                   */
+  const uint16_t *w_gate, *w_up, *w_down;    /* [E, f, d], [E, f, d], [E, d, f]          */
+  const uint16_t *ws_gate, *ws_up, *ws_down; /* shared [fs, d], [fs, d], [d, fs] or NULL  */
+  const float    *w_router, *router_bias;    /* [E, d], [E] or NULL                      */
+  const int32_t  *block_idx, *seq_offsets, *active_block;  /* budget path only           */
+  const uint8_t  *masked;
+  const int8_t   *hist_len;
+  const float    *conf_prev1, *conf_prev2;
+  const int32_t  *k_in;                      /* [T] or NULL                              */
+  const uint16_t *residual_a, *residual_b;   /* [T, d] bf16 added before rounding, or NULL */
+  reflex_alloc_params params;
+  uint16_t *out;                             /* [T, d] bf16                              */
+  int32_t  *k_out;                           /* [T] counts used, or NULL                 */
+  int32_t  *pairs_out;                       /* [1] P, or NULL                           */
+  float    *logits_out;                      /* [T, E] router scores, or NULL            */
+} reflex_moe_args;
+
+/* ws: >= reflex_workspace_size(T, E, d, f, f_shared, kcap) bytes, 256-byte aligned. */
+int reflex_moe_forward(const reflex_moe_args* args, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * reflex_moe_forward with timing marks, for benchmarks: identical work, plus
+ * hipEventRecord(stage_events[i], stream) at each stage boundary:
+ *   0 start, 1 router done, 2 counts done (budget / uniform fill / reuse),
+ *   3 count scan + TopK done, 4 permutation + GEMM tile plan done,
+ *   5 gate/up GEMM done, 6 down GEMM done, 7 shared expert done, 8 combine done.
+ * stage_events: host array of REFLEX_N_STAGE_EVENTS hipEvent_t handles created by
+ * the caller (hipEventCreate); the library only records them.
+ * Errors: as reflex_moe_forward; NULL stage_events or a NULL entry;
+ * n_stage_events != REFLEX_N_STAGE_EVENTS (REFLEX_ERR_SHAPE).
+ */
+#define REFLEX_N_STAGE_EVENTS 9
+int reflex_moe_forward_timed(const reflex_moe_args* args, void* ws, size_t ws_bytes, void* stream,
+                             void* const* stage_events, int n_stage_events);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* REFLEX_H */

@@ -1,0 +1,316 @@
+// C ABI of libreflex: host-side validation, workspace carving and launch order.
+// Every check happens before the first launch; nothing here allocates, frees or
+// synchronises.
+#include <cmath>
+#include <cstring>
+
+#include "common.h"
+
+using namespace rfx;
+
+namespace {
+
+constexpr int kVersion = 100;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_ptr(const void* p) {
+  if (p == nullptr) return REFLEX_ERR_NULL;
+  return aligned16(p) ? REFLEX_OK : REFLEX_ERR_SHAPE;
+}
+
+int check_opt_ptr(const void* p) { return (p == nullptr || aligned16(p)) ? REFLEX_OK : REFLEX_ERR_SHAPE; }
+
+#define RFX_TRY(expr)                 \
+  do {                                \
+    const int rc_ = (expr);           \
+    if (rc_ != REFLEX_OK) return rc_; \
+  } while (0)
+
+bool valid_T(int T) { return T >= 0 && T <= REFLEX_MAX_TOKENS; }
+bool valid_E(int E) { return E >= 1 && E <= REFLEX_MAX_EXPERTS; }
+bool valid_d(int d) { return d >= REFLEX_D_MULTIPLE && d <= REFLEX_MAX_DIM && d % REFLEX_D_MULTIPLE == 0; }
+bool valid_f(int f) { return f >= REFLEX_F_MULTIPLE && f <= REFLEX_MAX_DIM && f % REFLEX_F_MULTIPLE == 0; }
+bool valid_kmax(int k_max, int E) { return k_max >= 0 && k_max <= REFLEX_MAX_K && k_max <= E; }
+
+int check_params(const reflex_alloc_params* p) {
+  if (p == nullptr) return REFLEX_ERR_NULL;
+  const float fs[5] = {p->q, p->theta, p->w_cf, p->v_ref, p->tau};
+  for (float v : fs)
+    if (!std::isfinite(v)) return REFLEX_ERR_PARAM;
+  if (p->k_min < 0 || p->k_min > p->k_max || p->k_max > REFLEX_MAX_K) return REFLEX_ERR_PARAM;
+  if (p->k_base < 0 || p->delta_role < 0 || p->delta_cur < 0) return REFLEX_ERR_PARAM;
+  if (p->k_base > 1024 || p->delta_role > 1024 || p->delta_cur > 1024) return REFLEX_ERR_PARAM;
+  if (!(p->q > 0.0f && p->q <= 0.5f) || !(p->tau > 0.0f) || !(p->w_cf > 0.0f)) return REFLEX_ERR_PARAM;
+  if (p->signal < REFLEX_SIGNAL_FPS || p->signal > REFLEX_SIGNAL_UNCERTAINTY) return REFLEX_ERR_PARAM;
+  return REFLEX_OK;
+}
+
+// Fused-path workspace carve-up; every region 256-byte aligned.
+struct Layout {
+  size_t logits, k, scalar, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
+      pair_to_sorted, perm, swiglu, y, shared_act, shared_y, total;
+};
+
+bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
+  if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f)) return false;
+  if (fs != 0 && !valid_f(fs)) return false;
+  if (!valid_kmax(kcap, E)) return false;
+  const size_t cap = static_cast<size_t>(T) * kcap;
+  if (cap > static_cast<size_t>(INT32_MAX)) return false;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += align_up(bytes);
+    return at;
+  };
+  L.logits = take(sizeof(float) * static_cast<size_t>(T) * E);
+  L.k = take(sizeof(int32_t) * static_cast<size_t>(T));
+  L.scalar = take(sizeof(int32_t));
+  L.pair_offsets = take(sizeof(int32_t) * (static_cast<size_t>(T) + 1));
+  L.pair_expert = take(sizeof(int32_t) * cap);
+  L.pair_weight = take(sizeof(float) * cap);
+  L.expert_offsets = take(sizeof(int32_t) * (E + 1));
+  L.sorted_token = take(sizeof(int32_t) * cap);
+  L.pair_to_sorted = take(sizeof(int32_t) * cap);
+  L.perm = take(permute_ws_bytes(static_cast<int>(cap), E));
+  L.swiglu = take(swiglu_ws_bytes(static_cast<int>(cap), E, f));
+  L.y = take(sizeof(uint16_t) * cap * d);
+  L.shared_act = fs ? take(swiglu_dense_ws_bytes(T, fs)) : o;
+  L.shared_y = fs ? take(sizeof(uint16_t) * static_cast<size_t>(T) * d) : o;
+  L.total = o;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int reflex_version(void) { return kVersion; }
+
+const char* reflex_status_string(int status) {
+  switch (status) {
+    case REFLEX_OK: return "ok";
+    case REFLEX_ERR_NULL: return "null pointer";
+    case REFLEX_ERR_SHAPE: return "unsupported shape or misaligned pointer";
+    case REFLEX_ERR_PARAM: return "invalid hyper-parameter";
+    case REFLEX_ERR_WORKSPACE: return "workspace or pair capacity too small";
+    case REFLEX_ERR_LAUNCH: return "HIP launch error";
+    case REFLEX_ERR_UNSUPPORTED: return "unsupported request";
+    default: return "unknown status";
+  }
+}
+
+size_t reflex_sizeof_alloc_params(void) { return sizeof(reflex_alloc_params); }
+size_t reflex_sizeof_moe_args(void) { return sizeof(reflex_moe_args); }
+
+size_t reflex_workspace_size(int T, int E, int d, int f, int f_shared, int k_max) {
+  Layout L;
+  return make_layout(T, E, d, f, f_shared, k_max, L) ? L.total : 0;
+}
+
+size_t reflex_permute_workspace_size(int pair_capacity, int E) {
+  if (pair_capacity < 0 || !valid_E(E)) return 0;
+  return permute_ws_bytes(pair_capacity, E);
+}
+
+size_t reflex_swiglu_workspace_size(int pair_capacity, int E, int f) {
+  if (pair_capacity < 0 || !valid_E(E) || !valid_f(f)) return 0;
+  return swiglu_ws_bytes(pair_capacity, E, f);
+}
+
+int reflex_router_logits(const uint16_t* h, const float* w_router, const float* bias,
+                         float* logits, int T, int d, int E, void* stream) {
+  RFX_TRY(check_ptr(h));
+  RFX_TRY(check_ptr(w_router));
+  RFX_TRY(check_ptr(logits));
+  RFX_TRY(check_opt_ptr(bias));
+  if (!valid_T(T) || !valid_d(d) || !valid_E(E)) return REFLEX_ERR_SHAPE;
+  if (T == 0) return REFLEX_OK;
+  return launch_router(h, w_router, bias, logits, T, d, E, static_cast<hipStream_t>(stream));
+}
+
+int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
+                         const float* conf_prev1, const float* conf_prev2,
+                         const int32_t* seq_offsets, const int32_t* active_block, int B, int T,
+                         const reflex_alloc_params* params, int32_t* k_out, int32_t* pairs_out,
+                         double* fps_out, void* stream) {
+  const void* req[] = {block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offsets,
+                       active_block, k_out, pairs_out};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  RFX_TRY(check_opt_ptr(fps_out));
+  RFX_TRY(check_params(params));
+  if (!valid_T(T) || B < 0 || B > REFLEX_MAX_TOKENS || (T > 0 && B < 1)) return REFLEX_ERR_SHAPE;
+  if (T == 0) return REFLEX_OK;
+  return launch_budget(block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offsets,
+                       active_block, B, T, *params, k_out, pairs_out, fps_out,
+                       static_cast<hipStream_t>(stream));
+}
+
+int reflex_topk_variable(const float* logits, const int32_t* k, int T, int E, int k_max,
+                         int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
+                         float* pair_weight, int32_t pair_capacity, void* stream) {
+  const void* req[] = {logits, k, pair_offsets, pair_expert, pair_weight};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  if (!valid_T(T) || !valid_E(E) || !valid_kmax(k_max, E)) return REFLEX_ERR_SHAPE;
+  if (norm_topk != 0 && norm_topk != 1) return REFLEX_ERR_PARAM;
+  if (pair_capacity < 0 || static_cast<long long>(T) * k_max > pair_capacity) return REFLEX_ERR_WORKSPACE;
+  if (T == 0) return REFLEX_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  RFX_TRY(launch_count_scan(k, T, k_max, pair_offsets, nullptr, s));
+  return launch_topk(logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight, s);
+}
+
+int reflex_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
+                   int T, int E, int32_t pair_capacity, int32_t* expert_offsets,
+                   int32_t* sorted_token, int32_t* pair_to_sorted, void* ws, size_t ws_bytes,
+                   void* stream) {
+  const void* req[] = {pair_offsets, pair_expert, pairs, expert_offsets, sorted_token,
+                       pair_to_sorted, ws};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  if (!valid_T(T) || !valid_E(E) || pair_capacity < 0) return REFLEX_ERR_SHAPE;
+  if (ws_bytes < permute_ws_bytes(pair_capacity, E)) return REFLEX_ERR_WORKSPACE;
+  if (T == 0) return REFLEX_OK;
+  return launch_permute(pair_offsets, pair_expert, pairs, T, E, pair_capacity, expert_offsets,
+                        sorted_token, pair_to_sorted, ws, static_cast<hipStream_t>(stream));
+}
+
+int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
+                          const int32_t* expert_offsets, const uint16_t* w_gate,
+                          const uint16_t* w_up, const uint16_t* w_down, int T, int E, int d,
+                          int f, int32_t pair_capacity, uint16_t* y_sorted, void* ws,
+                          size_t ws_bytes, void* stream) {
+  const void* req[] = {h, sorted_token, expert_offsets, w_gate, w_up, w_down, y_sorted, ws};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || pair_capacity < 0)
+    return REFLEX_ERR_SHAPE;
+  if (ws_bytes < swiglu_ws_bytes(pair_capacity, E, f)) return REFLEX_ERR_WORKSPACE;
+  if (T == 0 || pair_capacity == 0) return REFLEX_OK;
+  return launch_swiglu_routed(h, sorted_token, expert_offsets, w_gate, w_up, w_down, T, E, d, f,
+                              pair_capacity, y_sorted, ws, static_cast<hipStream_t>(stream));
+}
+
+int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
+                   const int32_t* pair_to_sorted, const float* pair_weight,
+                   const uint16_t* shared_y, int T, int d, int32_t pair_capacity, uint16_t* out,
+                   void* stream) {
+  const void* req[] = {y_sorted, pair_offsets, pair_to_sorted, pair_weight, out};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  RFX_TRY(check_opt_ptr(shared_y));
+  if (!valid_T(T) || !valid_d(d) || pair_capacity < 0) return REFLEX_ERR_SHAPE;
+  if (T == 0) return REFLEX_OK;
+  return launch_combine(y_sorted, pair_offsets, pair_to_sorted, pair_weight, shared_y, nullptr,
+                        nullptr, T, d, pair_capacity, out, static_cast<hipStream_t>(stream));
+}
+
+static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream,
+                            void* const* ev) {
+  if (a == nullptr || ws == nullptr) return REFLEX_ERR_NULL;
+  const int T = a->T, E = a->E, d = a->d, f = a->f, fs = a->f_shared;
+  if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || fs < 0 || (fs && !valid_f(fs)))
+    return REFLEX_ERR_SHAPE;
+  if (a->norm_topk != 0 && a->norm_topk != 1) return REFLEX_ERR_PARAM;
+  const void* req[] = {a->h, a->w_gate, a->w_up, a->w_down, a->w_router, a->out, ws};
+  for (const void* p : req) RFX_TRY(check_ptr(p));
+  const void* opt[] = {a->router_bias, a->k_in, a->residual_a, a->residual_b, a->k_out,
+                       a->pairs_out, a->logits_out};
+  for (const void* p : opt) RFX_TRY(check_opt_ptr(p));
+  if (fs) {
+    RFX_TRY(check_ptr(a->ws_gate));
+    RFX_TRY(check_ptr(a->ws_up));
+    RFX_TRY(check_ptr(a->ws_down));
+  }
+  int kcap;
+  const bool budget = a->k_in == nullptr && a->uniform_k <= 0;
+  if (a->k_in == nullptr && a->uniform_k > 0) {
+    kcap = a->uniform_k;
+  } else {
+    RFX_TRY(check_params(&a->params));
+    kcap = a->params.k_max;
+  }
+  if (!valid_kmax(kcap, E)) return REFLEX_ERR_SHAPE;
+  if (budget) {
+    const void* st[] = {a->block_idx, a->seq_offsets, a->active_block, a->masked, a->hist_len,
+                        a->conf_prev1, a->conf_prev2};
+    for (const void* p : st) RFX_TRY(check_ptr(p));
+    if (a->B < 0 || a->B > REFLEX_MAX_TOKENS || (T > 0 && a->B < 1)) return REFLEX_ERR_SHAPE;
+  }
+  Layout L;
+  if (!make_layout(T, E, d, f, fs, kcap, L)) return REFLEX_ERR_SHAPE;
+  if (ws_bytes < L.total) return REFLEX_ERR_WORKSPACE;
+  if (T == 0) return REFLEX_OK;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto mark = [&](int i) {
+    if (ev && hipEventRecord(static_cast<hipEvent_t>(ev[i]), s) != hipSuccess) return REFLEX_ERR_LAUNCH;
+    return REFLEX_OK;
+  };
+  char* base = static_cast<char*>(ws);
+  auto at = [&](size_t off) { return static_cast<void*>(base + off); };
+  const int cap = T * kcap;
+  float* logits = a->logits_out ? a->logits_out : static_cast<float*>(at(L.logits));
+  int32_t* pair_offsets = static_cast<int32_t*>(at(L.pair_offsets));
+  int32_t* pair_expert = static_cast<int32_t*>(at(L.pair_expert));
+  float* pair_weight = static_cast<float*>(at(L.pair_weight));
+  int32_t* expert_offsets = static_cast<int32_t*>(at(L.expert_offsets));
+  int32_t* sorted_token = static_cast<int32_t*>(at(L.sorted_token));
+  int32_t* pair_to_sorted = static_cast<int32_t*>(at(L.pair_to_sorted));
+  uint16_t* y = static_cast<uint16_t*>(at(L.y));
+  void* gws = at(L.swiglu);
+
+  RFX_TRY(mark(0));
+  RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s));
+  RFX_TRY(mark(1));
+  const int32_t* k = a->k_in;
+  if (k == nullptr) {
+    int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
+    if (a->uniform_k > 0) {
+      RFX_TRY(launch_fill_i32(kb, a->uniform_k, T, s));
+    } else {
+      RFX_TRY(launch_budget(a->block_idx, a->masked, a->hist_len, a->conf_prev1, a->conf_prev2,
+                            a->seq_offsets, a->active_block, a->B, T, a->params, kb,
+                            static_cast<int32_t*>(at(L.scalar)), nullptr, s));
+    }
+    k = kb;
+  }
+  RFX_TRY(mark(2));
+  // P lives in pair_offsets[T]; the permutation reads it from there
+  RFX_TRY(launch_count_scan(k, T, kcap, pair_offsets, a->pairs_out, s));
+  RFX_TRY(launch_topk(logits, k, T, E, kcap, a->norm_topk, pair_offsets, pair_expert, pair_weight, s));
+  RFX_TRY(mark(3));
+  RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
+                         sorted_token, pair_to_sorted, at(L.perm), s));
+  RFX_TRY(launch_swiglu_plan(expert_offsets, E, gws, s));
+  RFX_TRY(mark(4));
+  RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up, T, E, d, f, cap,
+                           gws, s));
+  RFX_TRY(mark(5));
+  RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, E, d, f, cap, y, gws, s));
+  RFX_TRY(mark(6));
+  const uint16_t* shared_y = nullptr;
+  if (fs) {
+    uint16_t* sy = static_cast<uint16_t*>(at(L.shared_y));
+    RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, sy,
+                                at(L.shared_act), s));
+    shared_y = sy;
+  }
+  RFX_TRY(mark(7));
+  RFX_TRY(launch_combine(y, pair_offsets, pair_to_sorted, pair_weight, shared_y, a->residual_a,
+                         a->residual_b, T, d, cap, a->out, s));
+  return mark(8);
+}
+
+int reflex_moe_forward(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream) {
+  return moe_forward_impl(a, ws, ws_bytes, stream, nullptr);
+}
+
+int reflex_moe_forward_timed(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream,
+                             void* const* stage_events, int n_stage_events) {
+  if (stage_events == nullptr) return REFLEX_ERR_NULL;
+  if (n_stage_events != REFLEX_N_STAGE_EVENTS) return REFLEX_ERR_SHAPE;
+  for (int i = 0; i < n_stage_events; ++i)
+    if (stage_events[i] == nullptr) return REFLEX_ERR_NULL;
+  return moe_forward_impl(a, ws, ws_bytes, stream, stage_events);
+}
+
+}  // extern "C"

@@ -1,0 +1,136 @@
+// Internal helpers shared by the gfx950 kernels of libreflex (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "reflex.h"
+
+#define RFX_DEVICE __device__ __forceinline__
+
+namespace rfx {
+
+constexpr int kWave = 64;
+
+// ---- bf16 <-> fp32 ------------------------------------------------------------------
+RFX_DEVICE float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// Round to nearest, ties to even.  Inputs here are finite; NaN maps to a quiet NaN.
+RFX_DEVICE uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+RFX_DEVICE uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+// ---- wave64 reductions ----------------------------------------------------------------
+RFX_DEVICE int wave_sum_i32(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+RFX_DEVICE float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+RFX_DEVICE uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t w = __shfl_xor(v, o, kWave);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+RFX_DEVICE int wave_inclusive_scan_i32(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    int w = __shfl_up(v, o, kWave);
+    if (lane >= o) v += w;
+  }
+  return v;
+}
+
+// Order-preserving map of fp32 to uint32 (larger float -> larger key), with
+// -0.0 folded onto +0.0 so equal values tie.
+RFX_DEVICE uint32_t f32_order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+RFX_DEVICE float f32_from_order_key(uint32_t k) {
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(u);
+}
+
+RFX_DEVICE int clamp_count(int k, int k_max) { return k < 0 ? 0 : (k > k_max ? k_max : k); }
+
+}  // namespace rfx
+
+// ---- launch wrappers (host side, one per kernel family) ---------------------------------
+// Each returns REFLEX_OK or REFLEX_ERR_LAUNCH.  Arguments are already validated.
+namespace rfx {
+
+int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
+                  int d, int E, hipStream_t s);
+
+int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
+                  const float* c1, const float* c2, const int32_t* seq_offsets,
+                  const int32_t* active_block, int B, int T, const reflex_alloc_params& p,
+                  int32_t* k_out, int32_t* pairs_out, double* fps_out, hipStream_t s);
+
+int launch_fill_i32(int32_t* dst, int32_t value, int n, hipStream_t s);
+
+int launch_count_scan(const int32_t* k, int T, int k_max, int32_t* pair_offsets,
+                      int32_t* pairs_out, hipStream_t s);
+
+int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
+                const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
+                hipStream_t s);
+
+size_t permute_ws_bytes(int pair_capacity, int E);
+int launch_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
+                   int T, int E, int pair_capacity, int32_t* expert_offsets,
+                   int32_t* sorted_token, int32_t* pair_to_sorted, void* ws, hipStream_t s);
+
+size_t swiglu_ws_bytes(int pair_capacity, int E, int f);
+// Routed experts: rows grouped by expert_offsets, inputs gathered through sorted_token.
+int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
+                         const int32_t* expert_offsets, const uint16_t* wg, const uint16_t* wu,
+                         const uint16_t* wd, int T, int E, int d, int f, int pair_capacity,
+                         uint16_t* y_sorted, void* ws, hipStream_t s);
+// The same in three steps: per-expert M-tile plan, gate/up GEMM, down GEMM.
+int launch_swiglu_plan(const int32_t* expert_offsets, int E, void* ws, hipStream_t s);
+int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32_t* expert_offsets,
+                     const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
+                     void* ws, hipStream_t s);
+int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
+                       int cap, uint16_t* y_sorted, void* ws, hipStream_t s);
+// One dense expert over rows 0..M-1 of x (the always-on shared expert).
+size_t swiglu_dense_ws_bytes(int M, int f);
+int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* wu,
+                        const uint16_t* wd, int M, int d, int f, uint16_t* y, void* ws,
+                        hipStream_t s);
+
+int launch_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
+                   const int32_t* pair_to_sorted, const float* pair_weight,
+                   const uint16_t* shared_y, const uint16_t* res_a, const uint16_t* res_b,
+                   int T, int d, int pair_capacity, uint16_t* out, hipStream_t s);
+
+inline int launch_status() {
+  return hipGetLastError() == hipSuccess ? REFLEX_OK : REFLEX_ERR_LAUNCH;
+}
+
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+}  // namespace rfx

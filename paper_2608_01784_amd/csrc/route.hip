@@ -1,0 +1,239 @@
+// Variable-count TopK with routing weights (Section 3.2, Eq. (2)) and the
+// expert-sorted permutation of the selected expert-token pairs.
+#include "common.h"
+
+namespace rfx {
+namespace {
+
+// ------------------------------------------------------------------------------------
+// TopK: one wave per token.  Lane l holds experts l, l+64, l+128, l+192 as 64-bit
+// keys (order-preserving logit bits << 32 | (0xffff - expert)), so one unsigned
+// max selects the larger logit and, on equal logits, the lower expert index.
+// k_i rounds of wave-wide max pick the experts in rank order.
+// ------------------------------------------------------------------------------------
+constexpr int TK_WAVES = 4;
+
+__global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
+    const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
+    int norm_topk, const int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
+    float* __restrict__ pair_weight) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * TK_WAVES + (threadIdx.x >> 6);
+  if (i >= T) return;
+  const int ki = clamp_count(k[i], k_max);
+  if (ki == 0) return;
+  const float* row = logits + static_cast<size_t>(i) * E;
+  uint64_t key[4];
+  float val[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + kWave * j;
+    if (e < E) {
+      val[j] = row[e];
+      key[j] = (static_cast<uint64_t>(f32_order_key(val[j])) << 32) | (0xffffu - e);
+    } else {
+      val[j] = 0.0f;
+      key[j] = 0;
+    }
+  }
+  int my_e = 0;
+  float my_r = 0.0f, rmax = 0.0f;
+  for (int j = 0; j < ki; ++j) {
+    uint64_t best = key[0];
+#pragma unroll
+    for (int x = 1; x < 4; ++x) best = key[x] > best ? key[x] : best;
+    best = wave_max_u64(best);
+    const int e = 0xffff - static_cast<int>(best & 0xffffu);
+    const float r = f32_from_order_key(static_cast<uint32_t>(best >> 32));
+    if ((e & 63) == lane) key[e >> 6] = 0;     // consume the winner
+    if (lane == j) { my_e = e; my_r = r; }
+    if (j == 0) rmax = r;
+  }
+  float den;
+  if (norm_topk) {
+    den = wave_sum_f32(lane < ki ? expf(my_r - rmax) : 0.0f);
+  } else {
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (lane + kWave * j < E) part += expf(val[j] - rmax);
+    den = wave_sum_f32(part);
+  }
+  if (lane < ki) {
+    const int o = pair_offsets[i] + lane;
+    pair_expert[o] = my_e;
+    pair_weight[o] = expf(my_r - rmax) / den;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Permutation: stable counting sort of the token-major pair list by expert.
+//   1. per 4096-pair tile, an LDS histogram over experts
+//   2. one workgroup turns the [tile][expert] counts into start rows, expert-major
+//      then tile-minor, and writes expert_offsets
+//   3. per tile, 256-pair steps: each wave finds the lanes holding the same expert
+//      with eight ballots (one per bit of the expert id), ranks them by lane, and
+//      the waves of the step are ordered through LDS counts, so rows follow pair
+//      order within each expert (i.e. token order).
+// ------------------------------------------------------------------------------------
+constexpr int PM_TILE = 4096;
+constexpr int PM_THREADS = 256;
+constexpr int PM_STEPS = PM_TILE / PM_THREADS;
+
+__device__ __forceinline__ int pair_count(const int32_t* pairs, int cap) {
+  int P = *pairs;
+  return P < 0 ? 0 : (P > cap ? cap : P);
+}
+
+__global__ __launch_bounds__(PM_THREADS) void perm_hist_kernel(const int32_t* __restrict__ pair_expert,
+                                                               const int32_t* __restrict__ pairs,
+                                                               int cap, int E,
+                                                               int32_t* __restrict__ hist) {
+  __shared__ int cnt[REFLEX_MAX_EXPERTS];
+  const int P = pair_count(pairs, cap);
+  const int t = blockIdx.x, tid = threadIdx.x;
+  for (int e = tid; e < E; e += PM_THREADS) cnt[e] = 0;
+  __syncthreads();
+  const int begin = t * PM_TILE;
+  for (int j = 0; j < PM_STEPS; ++j) {
+    const int p = begin + j * PM_THREADS + tid;
+    if (p < P) {
+      int e = pair_expert[p];
+      e = e < 0 ? 0 : (e >= E ? E - 1 : e);
+      atomicAdd(&cnt[e], 1);
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += PM_THREADS) hist[static_cast<size_t>(t) * E + e] = cnt[e];
+}
+
+__global__ __launch_bounds__(PM_THREADS) void perm_scan_kernel(int32_t* __restrict__ hist,
+                                                               int n_tiles, int E,
+                                                               int32_t* __restrict__ expert_offsets) {
+  __shared__ int s_wave[PM_THREADS / kWave];
+  const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
+  int n = 0;
+  if (e < E)
+    for (int t = 0; t < n_tiles; ++t) n += hist[static_cast<size_t>(t) * E + e];
+  const int incl = wave_inclusive_scan_i32(n, lane);
+  if (lane == 63) s_wave[wv] = incl;
+  __syncthreads();
+  int base = incl - n;
+  for (int x = 0; x < wv; ++x) base += s_wave[x];
+  if (e < E) {
+    expert_offsets[e] = base;
+    if (e == E - 1) expert_offsets[E] = base + n;
+    int run = base;
+    for (int t = 0; t < n_tiles; ++t) {
+      const size_t x = static_cast<size_t>(t) * E + e;
+      const int c = hist[x];
+      hist[x] = run;
+      run += c;
+    }
+  }
+}
+
+// Largest token i in [lo, hi] with pair_offsets[i] <= p: the token that owns pair p.
+__device__ __forceinline__ int owner_token(const int32_t* __restrict__ off, int lo, int hi, int p) {
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= p) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
+    const int32_t* __restrict__ pair_offsets, const int32_t* __restrict__ pair_expert,
+    const int32_t* __restrict__ pairs, int T, int cap, int E, const int32_t* __restrict__ start,
+    int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted) {
+  __shared__ int run[REFLEX_MAX_EXPERTS];
+  __shared__ int wcnt[PM_THREADS / kWave][REFLEX_MAX_EXPERTS];
+  __shared__ int s_tok[2];
+  const int P = pair_count(pairs, cap);
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int begin = t * PM_TILE;
+  if (begin >= P) return;
+  for (int e = tid; e < E; e += PM_THREADS) {
+    run[e] = start[static_cast<size_t>(t) * E + e];
+#pragma unroll
+    for (int w = 0; w < PM_THREADS / kWave; ++w) wcnt[w][e] = 0;
+  }
+  if (tid == 0) {
+    const int last = (begin + PM_TILE < P ? begin + PM_TILE : P) - 1;
+    s_tok[0] = owner_token(pair_offsets, 0, T - 1, begin);
+    s_tok[1] = owner_token(pair_offsets, 0, T - 1, last);
+  }
+  __syncthreads();
+  const int tok_lo = s_tok[0], tok_hi = s_tok[1];
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  for (int j = 0; j < PM_STEPS; ++j) {
+    const int p = begin + j * PM_THREADS + tid;
+    const bool valid = p < P;
+    int e = 0, tok = 0;
+    if (valid) {
+      e = pair_expert[p];
+      e = e < 0 ? 0 : (e >= E ? E - 1 : e);
+      tok = owner_token(pair_offsets, tok_lo, tok_hi, p);
+    }
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (e >> b) & 1;
+      const uint64_t m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    const int local = __popcll(same & lt_mask);
+    if (valid && local == 0) wcnt[wv][e] = __popcll(same);
+    __syncthreads();
+    if (valid) {
+      int pos = run[e] + local;
+      for (int w = 0; w < wv; ++w) pos += wcnt[w][e];
+      sorted_token[pos] = tok;
+      pair_to_sorted[p] = pos;
+    }
+    __syncthreads();
+    for (int x = tid; x < E; x += PM_THREADS) {
+      int add = 0;
+#pragma unroll
+      for (int w = 0; w < PM_THREADS / kWave; ++w) {
+        add += wcnt[w][x];
+        wcnt[w][x] = 0;
+      }
+      run[x] += add;
+    }
+    __syncthreads();
+    if (begin + (j + 1) * PM_THREADS >= P) break;   // uniform across the workgroup
+  }
+}
+
+}  // namespace
+
+int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
+                const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
+                hipStream_t s) {
+  hipLaunchKernelGGL(topk_kernel, dim3((T + TK_WAVES - 1) / TK_WAVES), dim3(TK_WAVES * kWave), 0, s,
+                     logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight);
+  return launch_status();
+}
+
+static int perm_tiles(int cap) { return cap <= 0 ? 1 : (cap + PM_TILE - 1) / PM_TILE; }
+
+size_t permute_ws_bytes(int pair_capacity, int E) {
+  return align_up(static_cast<size_t>(perm_tiles(pair_capacity)) * E * sizeof(int32_t));
+}
+
+int launch_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
+                   int T, int E, int cap, int32_t* expert_offsets, int32_t* sorted_token,
+                   int32_t* pair_to_sorted, void* ws, hipStream_t s) {
+  const int n_tiles = perm_tiles(cap);
+  int32_t* hist = static_cast<int32_t*>(ws);
+  hipLaunchKernelGGL(perm_hist_kernel, dim3(n_tiles), dim3(PM_THREADS), 0, s, pair_expert, pairs,
+                     cap, E, hist);
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(PM_THREADS), 0, s, hist, n_tiles, E,
+                     expert_offsets);
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(PM_THREADS), 0, s, pair_offsets,
+                     pair_expert, pairs, T, cap, E, hist, sorted_token, pair_to_sorted);
+  return launch_status();
+}
+
+}  // namespace rfx
