@@ -22,8 +22,10 @@
  *    nothing is launched and a negative status is returned.  No C++ exception
  *    crosses the ABI.
  *  - T = 0 (no tokens) is valid and enqueues nothing.
- *  - Every device pointer must be 16-byte aligned (REFLEX_ERR_SHAPE otherwise);
- *    the kernels move data in 16-byte vectors.
+ *  - Alignment (REFLEX_ERR_SHAPE otherwise): bf16 matrices (h, expert weights,
+ *    y_sorted, shared_y, residuals, out), the fp32 router weight and workspaces
+ *    must be 16-byte aligned (the kernels move them in 16-byte vectors); every
+ *    other pointer needs the natural alignment of its element type.
  *  - Content preconditions that cannot be checked without reading device memory
  *    (seq_offsets non-decreasing from 0 to T, block_idx >= 0, hist_len in
  *    {0,1,2}, finite logits, expert_offsets consistent with the pair count) are

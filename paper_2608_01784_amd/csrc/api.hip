@@ -4,22 +4,40 @@
 #include <cmath>
 #include <cstring>
 
+#include <initializer_list>
+
 #include "common.h"
 
 using namespace rfx;
+
+#define RFX_TRY_INNER(expr)           \
+  do {                                \
+    const int rc_ = (expr);           \
+    if (rc_ != REFLEX_OK) return rc_; \
+  } while (0)
 
 namespace {
 
 constexpr int kVersion = 100;
 
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+// Pointers the kernels access with 16-byte vectors (bf16 matrices, the fp32 router
+// weight, the workspace) must be 16-byte aligned; every other pointer only needs the
+// natural alignment of its element type.
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-int check_ptr(const void* p) {
+int check_ptr(const void* p, size_t a = 16) {
   if (p == nullptr) return REFLEX_ERR_NULL;
-  return aligned16(p) ? REFLEX_OK : REFLEX_ERR_SHAPE;
+  return aligned(p, a) ? REFLEX_OK : REFLEX_ERR_SHAPE;
 }
 
-int check_opt_ptr(const void* p) { return (p == nullptr || aligned16(p)) ? REFLEX_OK : REFLEX_ERR_SHAPE; }
+int check_opt_ptr(const void* p, size_t a = 16) {
+  return (p == nullptr || aligned(p, a)) ? REFLEX_OK : REFLEX_ERR_SHAPE;
+}
+
+int check_ptrs(std::initializer_list<const void*> ps, size_t a) {
+  for (const void* p : ps) RFX_TRY_INNER(check_ptr(p, a));
+  return REFLEX_OK;
+}
 
 #define RFX_TRY(expr)                 \
   do {                                \
@@ -121,10 +139,9 @@ size_t reflex_swiglu_workspace_size(int pair_capacity, int E, int f) {
 
 int reflex_router_logits(const uint16_t* h, const float* w_router, const float* bias,
                          float* logits, int T, int d, int E, void* stream) {
-  RFX_TRY(check_ptr(h));
-  RFX_TRY(check_ptr(w_router));
-  RFX_TRY(check_ptr(logits));
-  RFX_TRY(check_opt_ptr(bias));
+  RFX_TRY(check_ptrs({h, w_router}, 16));
+  RFX_TRY(check_ptr(logits, 4));
+  RFX_TRY(check_opt_ptr(bias, 4));
   if (!valid_T(T) || !valid_d(d) || !valid_E(E)) return REFLEX_ERR_SHAPE;
   if (T == 0) return REFLEX_OK;
   return launch_router(h, w_router, bias, logits, T, d, E, static_cast<hipStream_t>(stream));
@@ -135,10 +152,10 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
                          const int32_t* seq_offsets, const int32_t* active_block, int B, int T,
                          const reflex_alloc_params* params, int32_t* k_out, int32_t* pairs_out,
                          double* fps_out, void* stream) {
-  const void* req[] = {block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offsets,
-                       active_block, k_out, pairs_out};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
-  RFX_TRY(check_opt_ptr(fps_out));
+  RFX_TRY(check_ptrs({masked, hist_len}, 1));
+  RFX_TRY(check_ptrs({block_idx, conf_prev1, conf_prev2, seq_offsets, active_block, k_out,
+                      pairs_out}, 4));
+  RFX_TRY(check_opt_ptr(fps_out, 8));
   RFX_TRY(check_params(params));
   if (!valid_T(T) || B < 0 || B > REFLEX_MAX_TOKENS || (T > 0 && B < 1)) return REFLEX_ERR_SHAPE;
   if (T == 0) return REFLEX_OK;
@@ -150,8 +167,7 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
 int reflex_topk_variable(const float* logits, const int32_t* k, int T, int E, int k_max,
                          int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
                          float* pair_weight, int32_t pair_capacity, void* stream) {
-  const void* req[] = {logits, k, pair_offsets, pair_expert, pair_weight};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
+  RFX_TRY(check_ptrs({logits, k, pair_offsets, pair_expert, pair_weight}, 4));
   if (!valid_T(T) || !valid_E(E) || !valid_kmax(k_max, E)) return REFLEX_ERR_SHAPE;
   if (norm_topk != 0 && norm_topk != 1) return REFLEX_ERR_PARAM;
   if (pair_capacity < 0 || static_cast<long long>(T) * k_max > pair_capacity) return REFLEX_ERR_WORKSPACE;
@@ -165,9 +181,9 @@ int reflex_permute(const int32_t* pair_offsets, const int32_t* pair_expert, cons
                    int T, int E, int32_t pair_capacity, int32_t* expert_offsets,
                    int32_t* sorted_token, int32_t* pair_to_sorted, void* ws, size_t ws_bytes,
                    void* stream) {
-  const void* req[] = {pair_offsets, pair_expert, pairs, expert_offsets, sorted_token,
-                       pair_to_sorted, ws};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
+  RFX_TRY(check_ptrs({pair_offsets, pair_expert, pairs, expert_offsets, sorted_token,
+                      pair_to_sorted}, 4));
+  RFX_TRY(check_ptr(ws, 16));
   if (!valid_T(T) || !valid_E(E) || pair_capacity < 0) return REFLEX_ERR_SHAPE;
   if (ws_bytes < permute_ws_bytes(pair_capacity, E)) return REFLEX_ERR_WORKSPACE;
   if (T == 0) return REFLEX_OK;
@@ -180,8 +196,8 @@ int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
                           const uint16_t* w_up, const uint16_t* w_down, int T, int E, int d,
                           int f, int32_t pair_capacity, uint16_t* y_sorted, void* ws,
                           size_t ws_bytes, void* stream) {
-  const void* req[] = {h, sorted_token, expert_offsets, w_gate, w_up, w_down, y_sorted, ws};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
+  RFX_TRY(check_ptrs({h, w_gate, w_up, w_down, y_sorted, ws}, 16));
+  RFX_TRY(check_ptrs({sorted_token, expert_offsets}, 4));
   if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || pair_capacity < 0)
     return REFLEX_ERR_SHAPE;
   if (ws_bytes < swiglu_ws_bytes(pair_capacity, E, f)) return REFLEX_ERR_WORKSPACE;
@@ -194,9 +210,9 @@ int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
                    const int32_t* pair_to_sorted, const float* pair_weight,
                    const uint16_t* shared_y, int T, int d, int32_t pair_capacity, uint16_t* out,
                    void* stream) {
-  const void* req[] = {y_sorted, pair_offsets, pair_to_sorted, pair_weight, out};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
-  RFX_TRY(check_opt_ptr(shared_y));
+  RFX_TRY(check_ptrs({y_sorted, out}, 16));
+  RFX_TRY(check_ptrs({pair_offsets, pair_to_sorted, pair_weight}, 4));
+  RFX_TRY(check_opt_ptr(shared_y, 16));
   if (!valid_T(T) || !valid_d(d) || pair_capacity < 0) return REFLEX_ERR_SHAPE;
   if (T == 0) return REFLEX_OK;
   return launch_combine(y_sorted, pair_offsets, pair_to_sorted, pair_weight, shared_y, nullptr,
@@ -210,16 +226,14 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || fs < 0 || (fs && !valid_f(fs)))
     return REFLEX_ERR_SHAPE;
   if (a->norm_topk != 0 && a->norm_topk != 1) return REFLEX_ERR_PARAM;
-  const void* req[] = {a->h, a->w_gate, a->w_up, a->w_down, a->w_router, a->out, ws};
-  for (const void* p : req) RFX_TRY(check_ptr(p));
-  const void* opt[] = {a->router_bias, a->k_in, a->residual_a, a->residual_b, a->k_out,
-                       a->pairs_out, a->logits_out};
-  for (const void* p : opt) RFX_TRY(check_opt_ptr(p));
-  if (fs) {
-    RFX_TRY(check_ptr(a->ws_gate));
-    RFX_TRY(check_ptr(a->ws_up));
-    RFX_TRY(check_ptr(a->ws_down));
-  }
+  RFX_TRY(check_ptrs({a->h, a->w_gate, a->w_up, a->w_down, a->w_router, a->out, ws}, 16));
+  for (const void* p : {static_cast<const void*>(a->residual_a), static_cast<const void*>(a->residual_b)})
+    RFX_TRY(check_opt_ptr(p, 16));
+  for (const void* p : {static_cast<const void*>(a->router_bias), static_cast<const void*>(a->k_in),
+                        static_cast<const void*>(a->k_out), static_cast<const void*>(a->pairs_out),
+                        static_cast<const void*>(a->logits_out)})
+    RFX_TRY(check_opt_ptr(p, 4));
+  if (fs) RFX_TRY(check_ptrs({a->ws_gate, a->ws_up, a->ws_down}, 16));
   int kcap;
   const bool budget = a->k_in == nullptr && a->uniform_k <= 0;
   if (a->k_in == nullptr && a->uniform_k > 0) {
@@ -230,9 +244,9 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   }
   if (!valid_kmax(kcap, E)) return REFLEX_ERR_SHAPE;
   if (budget) {
-    const void* st[] = {a->block_idx, a->seq_offsets, a->active_block, a->masked, a->hist_len,
-                        a->conf_prev1, a->conf_prev2};
-    for (const void* p : st) RFX_TRY(check_ptr(p));
+    RFX_TRY(check_ptrs({a->masked, a->hist_len}, 1));
+    RFX_TRY(check_ptrs({a->block_idx, a->seq_offsets, a->active_block, a->conf_prev1,
+                        a->conf_prev2}, 4));
     if (a->B < 0 || a->B > REFLEX_MAX_TOKENS || (T > 0 && a->B < 1)) return REFLEX_ERR_SHAPE;
   }
   Layout L;

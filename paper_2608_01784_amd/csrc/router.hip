@@ -1,72 +1,129 @@
-// Router scores r = h W_r^T (+ bias), Section 3.2.
+// Router scores r = h W_r^T (+ bias), Section 3.2, on bf16 MFMA.
 //
-// h is bf16 (widened exactly to fp32), W_r is fp32; every product is formed and
-// accumulated in fp32 with fused multiply-adds.  Each workgroup computes a
-// 64-token x 64-expert tile, staging 32-wide K slices of both operands in LDS.
+// h is bf16 and W_r is fp32.  Each fp32 weight is split exactly into three bf16
+// terms by truncation: hi = w with the low 16 bits cleared, mid = (w - hi) likewise,
+// lo = w - hi - mid (at most 8 significant bits left, so exact in bf16).  Every
+// product of a bf16 h with a bf16 term is exact in fp32, so three
+// v_mfma_f32_16x16x32_bf16 per K step give h . w with fp32 accumulation only.
+//
+// Workgroup tile: TM tokens x 64 experts, 4 waves.  The 64 x 32 slice of W_r for
+// each K step is loaded once per workgroup, split, and staged in LDS (double
+// buffered); h fragments are loaded straight from global memory.
+//   TM = 16: wave w computes the 16 tokens x experts 16w..16w+15   (small T)
+//   TM = 64: wave w computes tokens 16w..16w+15 x all 64 experts   (large T)
 #include "common.h"
 
 namespace rfx {
 namespace {
 
-constexpr int RT_TM = 64;   // tokens per tile
-constexpr int RT_TE = 64;   // experts per tile
-constexpr int RT_TK = 32;   // K slice
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void router_kernel(const uint16_t* __restrict__ h,
-                                                     const float* __restrict__ w,
-                                                     const float* __restrict__ bias,
-                                                     float* __restrict__ logits, int T, int d,
-                                                     int E) {
-  __shared__ float hs[RT_TK][RT_TM + 4];
-  __shared__ float wsm[RT_TK][RT_TE + 4];
-  const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * RT_TM;
-  const int e0 = blockIdx.y * RT_TE;
-  const int tx = tid & 15, ty = tid >> 4;     // 16 x 16 threads, 4 x 4 outputs each
+constexpr int RT_TE = 64;        // experts per workgroup
+constexpr int RT_TK = 32;        // K per MFMA step
+constexpr int RT_LDS = RT_TK + 8;  // padded row (bf16 elements)
 
-  // loader coordinates: 64 rows x 32 k = 256 threads x 8 consecutive k
-  const int lrow = tid >> 2, lk = (tid & 3) * 8;
-  const int tok = t0 + lrow, ex = e0 + lrow;
-  const bool tok_ok = tok < T, ex_ok = ex < E;
-  const uint16_t* hp = h + static_cast<size_t>(tok_ok ? tok : 0) * d + lk;
-  const float* wp = w + static_cast<size_t>(ex_ok ? ex : 0) * d + lk;
+__device__ __forceinline__ void split3(float w, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
+  const uint32_t u = __float_as_uint(w);
+  const uint32_t uh = u & 0xffff0000u;
+  const float r1 = w - __uint_as_float(uh);
+  const uint32_t um = __float_as_uint(r1) & 0xffff0000u;
+  const float r2 = r1 - __uint_as_float(um);
+  hi = static_cast<uint16_t>(uh >> 16);
+  mid = static_cast<uint16_t>(um >> 16);
+  lo = static_cast<uint16_t>(__float_as_uint(r2) >> 16);
+}
 
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < d; k0 += RT_TK) {
-    uint4 hv = tok_ok ? *reinterpret_cast<const uint4*>(hp + k0) : make_uint4(0, 0, 0, 0);
-    float4 wa = ex_ok ? *reinterpret_cast<const float4*>(wp + k0) : make_float4(0, 0, 0, 0);
-    float4 wb = ex_ok ? *reinterpret_cast<const float4*>(wp + k0 + 4) : make_float4(0, 0, 0, 0);
-    const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      hs[lk + 2 * j][lrow] = __uint_as_float(hw[j] << 16);
-      hs[lk + 2 * j + 1][lrow] = __uint_as_float(hw[j] & 0xffff0000u);
+template <int TM>
+__global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __restrict__ h,
+                                                          const float* __restrict__ w,
+                                                          const float* __restrict__ bias,
+                                                          float* __restrict__ logits, int T, int d,
+                                                          int E) {
+  constexpr int NB = TM == 16 ? 1 : 4;      // 16 x 16 accumulators per wave
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][RT_TE * RT_LDS];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int t0 = blockIdx.x * TM, e0 = blockIdx.y * RT_TE;
+
+  // W staging: thread -> expert tid/4, k chunk (tid%4)*8
+  const int se = tid >> 2, sk = (tid & 3) * 8;
+  const bool se_ok = e0 + se < E;
+  const float* wsrc = w + static_cast<size_t>(se_ok ? e0 + se : 0) * d + sk;
+  float4 wa, wb;
+  auto load_w = [&](int k0) {
+    if (se_ok) {
+      wa = *reinterpret_cast<const float4*>(wsrc + k0);
+      wb = *reinterpret_cast<const float4*>(wsrc + k0 + 4);
+    } else {
+      wa = make_float4(0, 0, 0, 0);
+      wb = wa;
     }
-    wsm[lk + 0][lrow] = wa.x; wsm[lk + 1][lrow] = wa.y; wsm[lk + 2][lrow] = wa.z; wsm[lk + 3][lrow] = wa.w;
-    wsm[lk + 4][lrow] = wb.x; wsm[lk + 5][lrow] = wb.y; wsm[lk + 6][lrow] = wb.z; wsm[lk + 7][lrow] = wb.w;
-    __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < RT_TK; ++kk) {
-      float a[4], b[4];
+  };
+  auto store_w = [&](int buf) {
+    const float v[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+    uint16_t t[3][8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = hs[kk][ty * 4 + i];
+    for (int j = 0; j < 8; ++j) split3(v[j], t[0][j], t[1][j], t[2][j]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = wsm[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(a[i], b[j], acc[i][j]);
+    for (int x = 0; x < 3; ++x) {
+      uint4 pk;
+      pk.x = t[x][0] | (uint32_t(t[x][1]) << 16);
+      pk.y = t[x][2] | (uint32_t(t[x][3]) << 16);
+      pk.z = t[x][4] | (uint32_t(t[x][5]) << 16);
+      pk.w = t[x][6] | (uint32_t(t[x][7]) << 16);
+      *reinterpret_cast<uint4*>(&Bs[buf][x][se * RT_LDS + sk]) = pk;
     }
+  };
+
+  // A fragments: lane holds token row (lane % 16) of its 16-token block, k (lane/16)*8..+8
+  const int tok_base = TM == 16 ? t0 : t0 + 16 * wv;
+  const int arow = lane & 15, ak = (lane >> 4) * 8;
+  const int tok = tok_base + arow;
+  const bool tok_ok = tok < T;
+  const uint16_t* asrc = h + static_cast<size_t>(tok_ok ? tok : 0) * d + ak;
+  uint4 afrag;
+  auto load_a = [&](int k0) {
+    afrag = tok_ok ? *reinterpret_cast<const uint4*>(asrc + k0) : make_uint4(0, 0, 0, 0);
+  };
+
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = d / RT_TK;
+  load_w(0);
+  load_a(0);
+  store_w(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, afrag);
+    if (kt + 1 < nk) {
+      load_w((kt + 1) * RT_TK);
+      load_a((kt + 1) * RT_TK);
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int erow = (TM == 16 ? 16 * wv : 16 * b) + (lane & 15);
+#pragma unroll
+      for (int x = 0; x < 3; ++x) {
+        const bf16x8_t bf = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][x][erow * RT_LDS + ak]);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf, acc[b], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < nk) store_w(buf ^ 1);
     __syncthreads();
   }
+  // accumulator: lane l, register r -> token row 4 (l/16) + r, expert column l % 16
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = t0 + ty * 4 + i;
-    if (t >= T) continue;
+  for (int b = 0; b < NB; ++b) {
+    const int e = e0 + (TM == 16 ? 16 * wv : 16 * b) + (lane & 15);
+    if (e >= E) continue;
+    const float be = bias ? bias[e] : 0.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = e0 + tx * 4 + j;
-      if (e < E) logits[static_cast<size_t>(t) * E + e] = acc[i][j] + (bias ? bias[e] : 0.0f);
+    for (int r = 0; r < 4; ++r) {
+      const int t = tok_base + 4 * (lane >> 4) + r;
+      if (t < T) logits[static_cast<size_t>(t) * E + e] = acc[b][r] + be;
     }
   }
 }
@@ -75,8 +132,14 @@ __global__ __launch_bounds__(256) void router_kernel(const uint16_t* __restrict_
 
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
                   int d, int E, hipStream_t s) {
-  dim3 grid((T + RT_TM - 1) / RT_TM, (E + RT_TE - 1) / RT_TE);
-  hipLaunchKernelGGL(router_kernel, grid, dim3(256), 0, s, h, w, bias, logits, T, d, E);
+  const int ne = (E + RT_TE - 1) / RT_TE;
+  if (T >= 4096) {
+    hipLaunchKernelGGL(router_mfma_kernel<64>, dim3((T + 63) / 64, ne), dim3(256), 0, s, h, w, bias,
+                       logits, T, d, E);
+  } else {
+    hipLaunchKernelGGL(router_mfma_kernel<16>, dim3((T + 15) / 16, ne), dim3(256), 0, s, h, w, bias,
+                       logits, T, d, E);
+  }
   return launch_status();
 }
 

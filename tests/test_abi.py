@@ -72,7 +72,8 @@ def test_workspace_sizes(L):
 
 
 FAKE = 1 << 20           # 16-byte aligned stand-in address, never dereferenced
-MIS = FAKE + 4           # misaligned
+MIS = FAKE + 4           # 4-byte aligned only: invalid for vector-accessed data
+ODD = FAKE + 2           # invalid for any 4-byte element type
 
 
 def good_params(**kw):
@@ -90,7 +91,9 @@ def test_router_validation(L):
     assert f(FAKE, FAKE, None, FAKE, 16, 256, 0, None) == -2
     assert f(FAKE, FAKE, None, FAKE, 16, 256, 257, None) == -2
     assert f(MIS, FAKE, None, FAKE, 16, 256, 8, None) == -2
-    assert f(FAKE, FAKE, MIS, FAKE, 16, 256, 8, None) == -2
+    assert f(FAKE, FAKE, ODD, FAKE, 16, 256, 8, None) == -2
+    assert f(FAKE, FAKE, None, ODD, 16, 256, 8, None) == -2
+    assert f(FAKE, MIS, None, FAKE, 16, 256, 8, None) == -2     # fp32 weight read as float4
     assert f(FAKE, FAKE, None, FAKE, 0, 256, 8, None) == 0      # empty: nothing launched
 
 
@@ -131,6 +134,10 @@ def test_permute_swiglu_combine_validation(L):
     need = L.reflex_permute_workspace_size(cap, E)
     assert L.reflex_permute(FAKE, FAKE, FAKE, 16, E, cap, FAKE, FAKE, FAKE, FAKE, need - 1, None) == -4
     assert L.reflex_permute(FAKE, FAKE, None, 16, E, cap, FAKE, FAKE, FAKE, FAKE, need, None) == -1
+    # a 4-byte-aligned scalar (e.g. pair_offsets + T) is a valid pair-count pointer
+    assert L.reflex_permute(FAKE, FAKE, MIS, 16, E, cap, FAKE, FAKE, FAKE, FAKE, need - 1, None) == -4
+    assert L.reflex_permute(FAKE, FAKE, ODD, 16, E, cap, FAKE, FAKE, FAKE, FAKE, need, None) == -2
+    assert L.reflex_permute(FAKE, FAKE, FAKE, 16, E, cap, FAKE, FAKE, FAKE, MIS, need, None) == -2
     assert L.reflex_permute(FAKE, FAKE, FAKE, 16, 0, cap, FAKE, FAKE, FAKE, FAKE, need, None) == -2
     need = L.reflex_swiglu_workspace_size(cap, E, f_)
     g = L.reflex_grouped_swiglu
