@@ -6,15 +6,27 @@
 //   up:   act[j, :] = SiLU(x_j W_gate[e]^T) * (x_j W_up[e]^T),  x_j = h[sorted_token[j]]
 //   down: y[j, :]   = act[j, :] W_down[e]^T
 // Rows of one expert are contiguous after the permutation; a device-side plan
-// cuts each expert's rows into 128-row M tiles, so the grid never depends on the
-// (device-resident) per-expert counts: workgroups past the last tile exit.
+// (tile_off) cuts each expert's rows into 128-row M tiles, so no launch shape
+// depends on the device-resident per-expert counts.
 //
-// Tile: 128 (M) x 128 (B rows) x 64 (K), 4 waves in 2 x 2, each wave 64 x 64 as
-// 2 x 2 v_mfma_f32_32x32x16_bf16 tiles, fp32 accumulators.  Operands are staged
-// through LDS with double buffering (rows padded to 144 bytes).  In the up GEMM
-// the 128 B rows are 64 gate rows and the 64 matching up rows, so gate and up of
-// the same output column land in the same lane and register, and SiLU(g) * u is
-// formed in registers before the single bf16 rounding of the activation.
+// Tile 128 (M) x 128 (B rows) x 64 (K); 4 waves in 2 x 2, each 64 x 64 as 2 x 2
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulators.  In the up GEMM the 128 B rows
+// are 64 gate rows followed by the 64 matching up rows, so gate and up of one
+// output column meet in the same lane and register and SiLU(g) * u is formed
+// before the single bf16 rounding of the activation.
+//
+// Data movement: operands go from global memory straight into LDS with
+// global_load_lds_dwordx4 (16 bytes per lane, no register staging) through a
+// ring of GM_STAGES K-slices, so GM_STAGES-1 slices are in flight while one is
+// multiplied.  Rows are 128 bytes (8 chunks of 16 bytes) with chunk c of row r
+// stored in slot c ^ (r % 8): a wave's 64 lanes write 1 KB contiguously and the
+// MFMA fragment reads of 8 consecutive rows hit 8 distinct bank groups.
+//
+// Scheduling: a persistent grid (one workgroup per CU) walks a flattened
+// sequence of (tile, K-slice) steps, so prefetching continues across tile
+// boundaries.  Tiles are dealt to the 8 XCDs in contiguous runs (workgroup b
+// runs on XCD b % 8), so one expert's tiles share that XCD's L2: the gathered
+// input rows and each weight tile are fetched from memory once.
 #include "common.h"
 
 namespace rfx {
@@ -25,43 +37,71 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int GM_BM = 128;
 constexpr int GM_BK = 64;
-constexpr int GM_LDS = GM_BK + 8;          // padded row, in bf16 elements (144 bytes)
 constexpr int GM_THREADS = 256;
 constexpr int GM_UP_BN = 64;               // activation columns per up-GEMM tile
 constexpr int GM_DOWN_BN = 128;            // output columns per down-GEMM tile
+constexpr int GM_TILE_ELEMS = GM_BM * GM_BK;   // one operand slice: 128 rows x 64 (16 KB)
+constexpr int GM_STAGES = 4;
+constexpr int GM_XCDS = 8;
 
-struct TileRange {
-  int row0, row_end, expert;
+struct Tile {
+  int expert, row0, row_end, n0;
 };
 
-// M tile -> (expert, first row, end row).  Routed mode searches the per-expert tile
-// prefix; dense mode (one expert over rows 0..M-1) has dense_M >= 0.
-// Rows are clamped to [0, out_rows) so inconsistent offsets can never index outside
-// the row buffers.
-__device__ __forceinline__ bool tile_range(int m_tile, const int32_t* __restrict__ tile_off,
-                                           const int32_t* __restrict__ expert_offsets, int E,
-                                           int dense_M, int out_rows, TileRange& tr) {
+// Logical tile L -> tile.  Routed: experts in order, within an expert the N tile
+// outer and the M tile inner (consecutive tiles share one weight slice).  Dense:
+// one expert over rows 0..dense_M-1.
+template <int BN>
+__device__ __forceinline__ Tile decode_tile(int L, const int32_t* __restrict__ tile_off,
+                                            const int32_t* __restrict__ expert_offsets, int E,
+                                            int dense_M, int n_tiles, int out_rows) {
+  Tile t;
   if (dense_M >= 0) {
-    tr.row0 = m_tile * GM_BM;
-    tr.row_end = dense_M;
-    tr.expert = 0;
-    return tr.row0 < dense_M;
+    const int mt = (dense_M + GM_BM - 1) / GM_BM;
+    t.expert = 0;
+    t.n0 = (L / mt) * BN;
+    t.row0 = (L % mt) * GM_BM;
+    t.row_end = dense_M;
+    return t;
   }
-  if (m_tile >= tile_off[E]) return false;
-  int lo = 0, hi = E - 1;               // largest e with tile_off[e] <= m_tile
+  int lo = 0, hi = E - 1;               // largest e with tile_off[e] * n_tiles <= L
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (tile_off[mid] <= m_tile) lo = mid; else hi = mid - 1;
+    if (tile_off[mid] * n_tiles <= L) lo = mid; else hi = mid - 1;
   }
-  tr.expert = lo;
-  tr.row0 = expert_offsets[lo] + (m_tile - tile_off[lo]) * GM_BM;
-  tr.row_end = expert_offsets[lo + 1] < out_rows ? expert_offsets[lo + 1] : out_rows;
-  return tr.row0 >= 0 && tr.row0 < tr.row_end;
+  const int local = L - tile_off[lo] * n_tiles;
+  const int mt = tile_off[lo + 1] - tile_off[lo];
+  t.expert = lo;
+  t.n0 = (local / mt) * BN;
+  t.row0 = expert_offsets[lo] + (local % mt) * GM_BM;
+  const int re = expert_offsets[lo + 1];
+  t.row_end = re < out_rows ? re : out_rows;
+  if (t.row0 < 0 || t.row0 >= t.row_end) t.row_end = t.row0;   // inconsistent offsets: no rows
+  return t;
+}
+
+// Each step issues 8 vector-memory ops per thread (4 A + 4 B); let the ops of
+// `pending` later steps stay outstanding.  gfx9 s_waitcnt immediate: vmcnt in
+// bits [3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] left at their maxima.
+__device__ __forceinline__ void wait_vm(int pending) {
+  if (pending <= 0) __builtin_amdgcn_s_waitcnt(0x0f70);                 // vmcnt(0)
+  else if (pending == 1) __builtin_amdgcn_s_waitcnt(0x0f78);            // vmcnt(8)
+  else __builtin_amdgcn_s_waitcnt(0x4f70);                              // vmcnt(16)
+}
+
+// Workgroup barrier without the release/acquire fences of __syncthreads(): those
+// would drain every outstanding vector-memory op (the in-flight LDS-DMA slices
+// included) at each step.  The explicit vmcnt wait before it already makes this
+// wave's DMA writes complete; lgkmcnt(0) makes this wave's earlier LDS reads
+// complete before any wave refills the slice they read; the memory clobber keeps
+// the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
-__global__ __launch_bounds__(GM_THREADS, 2) void swiglu_gemm_kernel(
+__global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
     const uint16_t* __restrict__ x,            // UP: h [T, K]; DOWN: act [rows, K]
     const int32_t* __restrict__ gather,        // UP: sorted_token or NULL (identity)
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ expert_offsets, int E,
@@ -69,71 +109,80 @@ __global__ __launch_bounds__(GM_THREADS, 2) void swiglu_gemm_kernel(
     const uint16_t* __restrict__ w1,                // UP: W_up
     size_t w_expert_stride, int K, int N_out, int x_rows, int out_rows,
     uint16_t* __restrict__ out) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][GM_BM * GM_LDS];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][GM_BM * GM_LDS];
-
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = N_out / BN;
-  const int m_tile = blockIdx.x / n_tiles;
-  const int n0 = (blockIdx.x % n_tiles) * BN;
-  TileRange tr;
-  if (!tile_range(m_tile, tile_off, expert_offsets, E, dense_M, out_rows, tr)) return;
+  const int total = dense_M >= 0 ? ((dense_M + GM_BM - 1) / GM_BM) * n_tiles : tile_off[E] * n_tiles;
 
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  // this workgroup's tiles: a contiguous run per XCD, strided over the XCD's workgroups
+  const int xcd = blockIdx.x % GM_XCDS;
+  const int per_xcd = gridDim.x / GM_XCDS;
+  const int j0 = blockIdx.x / GM_XCDS;
+  const int chunk = (total + GM_XCDS - 1) / GM_XCDS;
+  const int l_begin = xcd * chunk + j0;
+  const int l_end = min(total, (xcd + 1) * chunk);
+  if (l_begin >= l_end) return;
+  const int n_my = (l_end - l_begin + per_xcd - 1) / per_xcd;
+  const int nk = K / GM_BK;
+  const int n_steps = n_my * nk;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wv >> 1, wn = wv & 1;
 
-  // loader: 4 x 16-byte vectors of A and of B per thread; row (tid >> 3) + 32 j,
-  // column chunk (tid & 7) * 8
-  const int lcol = (tid & 7) * 8;
-  const uint16_t* a_src[4];
-  const uint16_t* b_src[4];
-  bool a_ok[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = (tid >> 3) + 32 * j;
-    const int grow = tr.row0 + r;
-    a_ok[j] = grow < tr.row_end;
-    int src_row = a_ok[j] ? grow : tr.row0;
-    if (UP && gather != nullptr) {
-      src_row = gather[src_row];
-      src_row = src_row < 0 ? 0 : (src_row >= x_rows ? x_rows - 1 : src_row);
-    }
-    a_src[j] = x + static_cast<size_t>(src_row) * K + lcol;
-    const uint16_t* wbase;
-    int wrow;
-    if (UP) {
-      wbase = (r < 64 ? w0 : w1) + tr.expert * w_expert_stride;
-      wrow = n0 + (r & 63);
-    } else {
-      wbase = w0 + tr.expert * w_expert_stride;
-      wrow = n0 + r;
-    }
-    b_src[j] = wbase + static_cast<size_t>(wrow) * K + lcol;
-  }
-
-  uint4 ra[4], rb[4];
-  auto load_global = [&](int k0) {
+  // ---- loader (runs GM_STAGES-1 steps ahead of the multiply) ----
+  // lane L of wave w, op j (0..3) fills row r = (4w + j) * 8 + L / 8, slot L % 8,
+  // which holds logical chunk c = (L % 8) ^ (r % 8) = (L % 8) ^ (L / 8)
+  const int l_chunk = ((lane & 7) ^ (lane >> 3)) * 8;
+  const uint16_t* a_ptr[4];
+  const uint16_t* b_ptr[4];
+  int ld_tile = -1;
+  auto setup_loader = [&](int tile_i) {
+    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E, dense_M,
+                                   n_tiles, out_rows);
+    const int rows_valid = t.row_end - t.row0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      ra[j] = a_ok[j] ? *reinterpret_cast<const uint4*>(a_src[j] + k0) : make_uint4(0, 0, 0, 0);
-      rb[j] = *reinterpret_cast<const uint4*>(b_src[j] + k0);
+      const int r = (4 * wv + j) * 8 + (lane >> 3);
+      int src = t.row0 + (r < rows_valid ? r : 0);     // rows past the expert reuse row0
+      if (rows_valid <= 0) src = 0;
+      if (UP && gather != nullptr) {
+        src = gather[src];
+        src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
+      }
+      a_ptr[j] = x + static_cast<size_t>(src) * K + l_chunk;
+      const uint16_t* wb;
+      int wr;
+      if (UP) {
+        wb = (r < 64 ? w0 : w1) + t.expert * w_expert_stride;
+        wr = t.n0 + (r & 63);
+      } else {
+        wb = w0 + t.expert * w_expert_stride;
+        wr = t.n0 + r;
+      }
+      b_ptr[j] = wb + static_cast<size_t>(wr) * K + l_chunk;
     }
   };
-  auto store_lds = [&](int buf) {
+  auto issue = [&](int step) {
+    const int tile_i = step / nk, kt = step - tile_i * nk;
+    if (tile_i != ld_tile) {
+      setup_loader(tile_i);
+      ld_tile = tile_i;
+    }
+    uint16_t* As = smem + (step % GM_STAGES) * 2 * GM_TILE_ELEMS;
+    uint16_t* Bs = As + GM_TILE_ELEMS;
+    const int k0 = kt * GM_BK;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = (tid >> 3) + 32 * j;
-      *reinterpret_cast<uint4*>(&As[buf][r * GM_LDS + lcol]) = ra[j];
-      *reinterpret_cast<uint4*>(&Bs[buf][r * GM_LDS + lcol]) = rb[j];
+      __builtin_amdgcn_global_load_lds(a_ptr[j] + k0, As + (4 * wv + j) * 512, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(b_ptr[j] + k0, Bs + (4 * wv + j) * 512, 16, 0, 0);
     }
   };
 
-  // B sub-tile rows of this wave: UP -> gate rows wn*32.., up rows 64 + wn*32..;
-  // DOWN -> rows wn*64 and wn*64 + 32
+  // ---- multiply ----
   const int b_row[2] = {UP ? wn * 32 : wn * 64, UP ? 64 + wn * 32 : wn * 64 + 32};
   const int a_row[2] = {wm * 64, wm * 64 + 32};
-  const int frag_row = lane & 31, frag_k = (lane >> 5) * 8;
-
+  const int frow = lane & 31, fsel = lane >> 5, fx = lane & 7;
   f32x16_t acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -142,51 +191,53 @@ __global__ __launch_bounds__(GM_THREADS, 2) void swiglu_gemm_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = K / GM_BK;
-  load_global(0);
-  store_lds(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_global((kt + 1) * GM_BK);
+  for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
+  for (int s = 0; s < n_steps; ++s) {
+    wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
+    lds_barrier();         // slice s visible to all waves; slice s-1 no longer read
+    if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
+    const uint16_t* As = smem + (s % GM_STAGES) * 2 * GM_TILE_ELEMS;
+    const uint16_t* Bs = As + GM_TILE_ELEMS;
 #pragma unroll
     for (int kk = 0; kk < GM_BK / 16; ++kk) {
+      const int slot = ((2 * kk + fsel) ^ fx) * 8;
       bf16x8_t af[2], bfr[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(
-            &As[buf][(a_row[i] + frag_row) * GM_LDS + kk * 16 + frag_k]);
+        af[i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(
-            &Bs[buf][(b_row[j] + frag_row) * GM_LDS + kk * 16 + frag_k]);
+        bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_lds(buf ^ 1);
-    __syncthreads();
-  }
-
-  // epilogue: acc lane l, register r holds row 8 (r/4) + 4 (l/32) + r%4, column l%32
-  const int col = lane & 31;
+    const int tile_i = s / nk;
+    if (s - tile_i * nk == nk - 1) {
+      // epilogue: lane l, register r holds row 8 (r/4) + 4 (l/32) + r%4, column l%32
+      const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E,
+                                     dense_M, n_tiles, out_rows);
+      const int col = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < 2; ++i) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int mrow = a_row[i] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int grow = tr.row0 + mrow;
-      if (grow >= tr.row_end) continue;
-      uint16_t* orow = out + static_cast<size_t>(grow) * N_out + n0;
-      if (UP) {
-        const float g = acc[i][0][r], u = acc[i][1][r];
-        const float a = g / (1.0f + expf(-g)) * u;
-        orow[wn * 32 + col] = f32_to_bf16(a);
-      } else {
-        orow[wn * 64 + col] = f32_to_bf16(acc[i][0][r]);
-        orow[wn * 64 + 32 + col] = f32_to_bf16(acc[i][1][r]);
+        for (int r = 0; r < 16; ++r) {
+          const int grow = t.row0 + a_row[i] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (grow < t.row_end) {
+            uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
+            if (UP) {
+              const float g = acc[i][0][r], u = acc[i][1][r];
+              orow[wn * 32 + col] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+            } else {
+              orow[wn * 64 + col] = f32_to_bf16(acc[i][0][r]);
+              orow[wn * 64 + 32 + col] = f32_to_bf16(acc[i][1][r]);
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j][r] = 0.0f;
+        }
       }
     }
   }
@@ -213,10 +264,40 @@ __global__ __launch_bounds__(256) void tile_plan_kernel(const int32_t* __restric
   }
 }
 
-int max_m_tiles(int cap, int E) {
-  long long t = (static_cast<long long>(cap) + GM_BM - 1) / GM_BM + E;
-  if (t > cap) t = cap;
-  return static_cast<int>(t < 1 ? 1 : t);
+constexpr size_t kGemmLds = size_t(GM_STAGES) * 2 * GM_TILE_ELEMS * sizeof(uint16_t);
+
+// One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
+// a multiple of the XCD count.
+int persistent_grid() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return (cus + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
+}
+
+template <bool UP>
+int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_off,
+                const int32_t* eo, int E, int dense_M, const uint16_t* w0, const uint16_t* w1,
+                size_t stride, int K, int N, int x_rows, int out_rows, uint16_t* out,
+                hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&swiglu_gemm_kernel<UP>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(kGemmLds)) != hipSuccess)
+      return REFLEX_ERR_LAUNCH;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(swiglu_gemm_kernel<UP>, dim3(persistent_grid()), dim3(GM_THREADS), kGemmLds, s,
+                     x, gather, tile_off, eo, E, dense_M, w0, w1, stride, K, N, x_rows, out_rows,
+                     out);
+  return launch_status();
 }
 
 }  // namespace
@@ -244,23 +325,16 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
                      const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
                      void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  const int32_t* tile_off = static_cast<const int32_t*>(ws);
-  const int mt = max_m_tiles(cap, E);
-  hipLaunchKernelGGL(swiglu_gemm_kernel<true>, dim3(mt * (f / GM_UP_BN)), dim3(GM_THREADS), 0, s,
-                     h, sorted_token, tile_off, expert_offsets, E, -1, wg, wu,
-                     static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E));
-  return launch_status();
+  return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
+                           wg, wu, static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
 }
 
 int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
                        int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  const int32_t* tile_off = static_cast<const int32_t*>(ws);
-  const int mt = max_m_tiles(cap, E);
-  hipLaunchKernelGGL(swiglu_gemm_kernel<false>, dim3(mt * (d / GM_DOWN_BN)), dim3(GM_THREADS), 0,
-                     s, routed_act(ws, E), nullptr, tile_off, expert_offsets, E, -1, wd, nullptr,
-                     static_cast<size_t>(d) * f, f, d, cap, cap, y_sorted);
-  return launch_status();
+  return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
+                            expert_offsets, E, -1, wd, nullptr, static_cast<size_t>(d) * f, f, d,
+                            cap, cap, y_sorted, s);
 }
 
 int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
@@ -279,12 +353,10 @@ int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* w
                         hipStream_t s) {
   if (M <= 0) return REFLEX_OK;
   uint16_t* act = static_cast<uint16_t*>(ws);
-  const int mt = (M + GM_BM - 1) / GM_BM;
-  hipLaunchKernelGGL(swiglu_gemm_kernel<true>, dim3(mt * (f / GM_UP_BN)), dim3(GM_THREADS), 0, s,
-                     x, nullptr, nullptr, nullptr, 1, M, wg, wu, size_t(0), d, f, M, M, act);
-  hipLaunchKernelGGL(swiglu_gemm_kernel<false>, dim3(mt * (d / GM_DOWN_BN)), dim3(GM_THREADS), 0,
-                     s, act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, size_t(0), f, d, M, M, y);
-  return launch_status();
+  int rc = launch_gemm<true>(x, nullptr, nullptr, nullptr, 1, M, wg, wu, 0, d, f, M, M, act, s);
+  if (rc == REFLEX_OK)
+    rc = launch_gemm<false>(act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, 0, f, d, M, M, y, s);
+  return rc;
 }
 
 }  // namespace rfx
