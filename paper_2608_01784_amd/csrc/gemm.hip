@@ -9,11 +9,13 @@
 // (tile_off) cuts each expert's rows into 128-row M tiles, so no launch shape
 // depends on the device-resident per-expert counts.
 //
-// Tile 128 (M) x 128 (B rows) x 64 (K); 4 waves in 2 x 2, each 64 x 64 as 2 x 2
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulators.  In the up GEMM the 128 B rows
-// are 64 gate rows followed by the 64 matching up rows, so gate and up of one
-// output column meet in the same lane and register and SiLU(g) * u is formed
-// before the single bf16 rounding of the activation.
+// Tile 128 (M) x GM_BROWS (weight rows, 256) x 64 (K); 4 waves in 2 x 2, each
+// 64 x GM_BROWS/2 as 2 x GM_NT v_mfma_f32_32x32x16_bf16 tiles with fp32
+// accumulators.  In the up GEMM the first half of the weight rows are gate rows and
+// the second half the matching up rows, so gate and up of one output column meet
+// in the same lane and register and SiLU(g) * u is formed before the single bf16
+// rounding of the activation.  A partial last N tile clamps its weight rows and
+// skips the stores past N.
 //
 // Data movement: operands go from global memory straight into LDS with
 // global_load_lds_dwordx4 (16 bytes per lane, no register staging) through a
@@ -35,14 +37,26 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+#ifndef RFX_GEMM_BROWS
+#define RFX_GEMM_BROWS 256
+#endif
+#ifndef RFX_GEMM_STAGES
+#define RFX_GEMM_STAGES 3
+#endif
 constexpr int GM_BM = 128;
 constexpr int GM_BK = 64;
 constexpr int GM_THREADS = 256;
-constexpr int GM_UP_BN = 64;               // activation columns per up-GEMM tile
-constexpr int GM_DOWN_BN = 128;            // output columns per down-GEMM tile
-constexpr int GM_TILE_ELEMS = GM_BM * GM_BK;   // one operand slice: 128 rows x 64 (16 KB)
-constexpr int GM_STAGES = 4;
+constexpr int GM_BROWS = RFX_GEMM_BROWS;   // weight (B) rows per tile: 128 or 256
+constexpr int GM_UP_BN = GM_BROWS / 2;     // activation columns per up-GEMM tile (gate + up rows)
+constexpr int GM_DOWN_BN = GM_BROWS;       // output columns per down-GEMM tile
+constexpr int GM_A_ELEMS = GM_BM * GM_BK;      // A slice: 128 rows x 64
+constexpr int GM_B_ELEMS = GM_BROWS * GM_BK;   // B slice
+constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
+constexpr int GM_STAGES = RFX_GEMM_STAGES;
 constexpr int GM_XCDS = 8;
+constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per wave
+constexpr int GM_B_OPS = GM_BROWS / 32;    // 8-row DMA ops per wave for B
+constexpr int GM_OPS = 4 + GM_B_OPS;       // vector-memory ops per thread per step
 
 struct Tile {
   int expert, row0, row_end, n0;
@@ -80,13 +94,25 @@ __device__ __forceinline__ Tile decode_tile(int L, const int32_t* __restrict__ t
   return t;
 }
 
-// Each step issues 8 vector-memory ops per thread (4 A + 4 B); let the ops of
-// `pending` later steps stay outstanding.  gfx9 s_waitcnt immediate: vmcnt in
-// bits [3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] left at their maxima.
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt left at their maxima (gfx9 encoding:
+// vmcnt in bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
+}
+
+// Each step issues GM_OPS vector-memory ops per thread; let the ops of `pending`
+// later steps stay outstanding.
 __device__ __forceinline__ void wait_vm(int pending) {
-  if (pending <= 0) __builtin_amdgcn_s_waitcnt(0x0f70);                 // vmcnt(0)
-  else if (pending == 1) __builtin_amdgcn_s_waitcnt(0x0f78);            // vmcnt(8)
-  else __builtin_amdgcn_s_waitcnt(0x4f70);                              // vmcnt(16)
+  static_assert(GM_STAGES >= 2 && GM_STAGES <= 6, "stage count");
+  switch (pending) {
+    case 0: waitcnt_vm<0>(); break;
+    case 1: waitcnt_vm<GM_OPS>(); break;
+    case 2: waitcnt_vm<(GM_STAGES > 3 ? 2 * GM_OPS : 0)>(); break;
+    case 3: waitcnt_vm<(GM_STAGES > 4 ? 3 * GM_OPS : 0)>(); break;
+    default: waitcnt_vm<(GM_STAGES > 5 ? 4 * GM_OPS : 0)>(); break;
+  }
 }
 
 // Workgroup barrier without the release/acquire fences of __syncthreads(): those
@@ -111,7 +137,7 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
     uint16_t* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
-  const int n_tiles = N_out / BN;
+  const int n_tiles = (N_out + BN - 1) / BN;     // the last N tile may be partial
   const int total = dense_M >= 0 ? ((dense_M + GM_BM - 1) / GM_BM) * n_tiles : tile_off[E] * n_tiles;
 
   // this workgroup's tiles: a contiguous run per XCD, strided over the XCD's workgroups
@@ -135,7 +161,7 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
   // which holds logical chunk c = (L % 8) ^ (r % 8) = (L % 8) ^ (L / 8)
   const int l_chunk = ((lane & 7) ^ (lane >> 3)) * 8;
   const uint16_t* a_ptr[4];
-  const uint16_t* b_ptr[4];
+  const uint16_t* b_ptr[GM_B_OPS];
   int ld_tile = -1;
   auto setup_loader = [&](int tile_i) {
     const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E, dense_M,
@@ -151,15 +177,20 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
         src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
       }
       a_ptr[j] = x + static_cast<size_t>(src) * K + l_chunk;
+    }
+#pragma unroll
+    for (int j = 0; j < GM_B_OPS; ++j) {
+      const int r = (GM_B_OPS * wv + j) * 8 + (lane >> 3);
       const uint16_t* wb;
       int wr;
-      if (UP) {
-        wb = (r < 64 ? w0 : w1) + t.expert * w_expert_stride;
-        wr = t.n0 + (r & 63);
+      if (UP) {     // rows [0, BROWS/2): gate rows n0 + r; the rest: up rows n0 + r - BROWS/2
+        wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
+        wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
       } else {
         wb = w0 + t.expert * w_expert_stride;
         wr = t.n0 + r;
       }
+      wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
       b_ptr[j] = wb + static_cast<size_t>(wr) * K + l_chunk;
     }
   };
@@ -169,25 +200,34 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
       setup_loader(tile_i);
       ld_tile = tile_i;
     }
-    uint16_t* As = smem + (step % GM_STAGES) * 2 * GM_TILE_ELEMS;
-    uint16_t* Bs = As + GM_TILE_ELEMS;
+    uint16_t* As = smem + (step % GM_STAGES) * GM_STAGE_ELEMS;
+    uint16_t* Bs = As + GM_A_ELEMS;
     const int k0 = kt * GM_BK;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 4; ++j)
       __builtin_amdgcn_global_load_lds(a_ptr[j] + k0, As + (4 * wv + j) * 512, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(b_ptr[j] + k0, Bs + (4 * wv + j) * 512, 16, 0, 0);
-    }
+#pragma unroll
+    for (int j = 0; j < GM_B_OPS; ++j)
+      __builtin_amdgcn_global_load_lds(b_ptr[j] + k0, Bs + (GM_B_OPS * wv + j) * 512, 16, 0, 0);
   };
 
   // ---- multiply ----
-  const int b_row[2] = {UP ? wn * 32 : wn * 64, UP ? 64 + wn * 32 : wn * 64 + 32};
+  // B sub-tiles of this wave (32 rows each).  UP: the first GM_NT/2 are gate rows
+  // wn*BROWS/4 + 32j, the rest the matching up rows (+ BROWS/2), so sub-tile j and
+  // j + GM_NT/2 hold gate and up of the same output columns.  DOWN: wn*BROWS/2 + 32j.
+  int b_row[GM_NT];
+#pragma unroll
+  for (int j = 0; j < GM_NT; ++j)
+    b_row[j] = UP ? (j < GM_NT / 2 ? wn * (GM_BROWS / 4) + 32 * j
+                                   : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - GM_NT / 2))
+                  : wn * (GM_BROWS / 2) + 32 * j;
   const int a_row[2] = {wm * 64, wm * 64 + 32};
   const int frow = lane & 31, fsel = lane >> 5, fx = lane & 7;
-  f32x16_t acc[2][2];
+  f32x16_t acc[2][GM_NT];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < GM_NT; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -196,22 +236,22 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
     wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
     lds_barrier();         // slice s visible to all waves; slice s-1 no longer read
     if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
-    const uint16_t* As = smem + (s % GM_STAGES) * 2 * GM_TILE_ELEMS;
-    const uint16_t* Bs = As + GM_TILE_ELEMS;
+    const uint16_t* As = smem + (s % GM_STAGES) * GM_STAGE_ELEMS;
+    const uint16_t* Bs = As + GM_A_ELEMS;
 #pragma unroll
     for (int kk = 0; kk < GM_BK / 16; ++kk) {
       const int slot = ((2 * kk + fsel) ^ fx) * 8;
-      bf16x8_t af[2], bfr[2];
+      bf16x8_t af[2], bfr[GM_NT];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
         af[i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < GM_NT; ++j)
         bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < GM_NT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
     const int tile_i = s / nk;
@@ -228,15 +268,22 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
           if (grow < t.row_end) {
             uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
             if (UP) {
-              const float g = acc[i][0][r], u = acc[i][1][r];
-              orow[wn * 32 + col] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+#pragma unroll
+              for (int j = 0; j < GM_NT / 2; ++j) {
+                const int c = wn * (GM_BROWS / 4) + 32 * j + col;
+                const float g = acc[i][j][r], u = acc[i][j + GM_NT / 2][r];
+                if (t.n0 + c < N_out) orow[c] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+              }
             } else {
-              orow[wn * 64 + col] = f32_to_bf16(acc[i][0][r]);
-              orow[wn * 64 + 32 + col] = f32_to_bf16(acc[i][1][r]);
+#pragma unroll
+              for (int j = 0; j < GM_NT; ++j) {
+                const int c = wn * (GM_BROWS / 2) + 32 * j + col;
+                if (t.n0 + c < N_out) orow[c] = f32_to_bf16(acc[i][j][r]);
+              }
             }
           }
 #pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j][r] = 0.0f;
+          for (int j = 0; j < GM_NT; ++j) acc[i][j][r] = 0.0f;
         }
       }
     }
@@ -264,7 +311,7 @@ __global__ __launch_bounds__(256) void tile_plan_kernel(const int32_t* __restric
   }
 }
 
-constexpr size_t kGemmLds = size_t(GM_STAGES) * 2 * GM_TILE_ELEMS * sizeof(uint16_t);
+constexpr size_t kGemmLds = size_t(GM_STAGES) * GM_STAGE_ELEMS * sizeof(uint16_t);
 
 // One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
 // a multiple of the XCD count.
