@@ -21,8 +21,10 @@
 // global_load_lds_dwordx4 (16 bytes per lane, no register staging) through a
 // ring of GM_STAGES K-slices, so GM_STAGES-1 slices are in flight while one is
 // multiplied.  Rows are 128 bytes (8 chunks of 16 bytes) with chunk c of row r
-// stored in slot c ^ (r % 8): a wave's 64 lanes write 1 KB contiguously and the
-// MFMA fragment reads of 8 consecutive rows hit 8 distinct bank groups.
+// stored in slot c ^ ((r / 2) % 8).  The LDS has 64 four-byte banks and serves a
+// 16-byte read for 16 lanes at a time, i.e. 16 rows of one fragment: their
+// (row parity, slot) pairs are all distinct, so fragment reads are conflict-free,
+// while a wave's DMA still writes 1 KB (8 whole rows) contiguously.
 //
 // Scheduling: a persistent grid (one workgroup per CU) walks a flattened
 // sequence of (tile, K-slice) steps, so prefetching continues across tile
@@ -157,9 +159,10 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
   const int wm = wv >> 1, wn = wv & 1;
 
   // ---- loader (runs GM_STAGES-1 steps ahead of the multiply) ----
-  // lane L of wave w, op j (0..3) fills row r = (4w + j) * 8 + L / 8, slot L % 8,
-  // which holds logical chunk c = (L % 8) ^ (r % 8) = (L % 8) ^ (L / 8)
-  const int l_chunk = ((lane & 7) ^ (lane >> 3)) * 8;
+  // op q of a wave fills rows R0 = 8 q' .. 8 q' + 7 (q' the op's global 8-row index);
+  // lane L writes row r = R0 + L / 8, slot L % 8, which must hold logical chunk
+  // c = (L % 8) ^ ((r / 2) % 8) = (L % 8) ^ (4 (q' % 2) + L / 16).
+  auto lane_chunk = [&](int q) { return ((lane & 7) ^ (((q & 1) << 2) | (lane >> 4))) * 8; };
   const uint16_t* a_ptr[4];
   const uint16_t* b_ptr[GM_B_OPS];
   int ld_tile = -1;
@@ -176,7 +179,7 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
         src = gather[src];
         src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
       }
-      a_ptr[j] = x + static_cast<size_t>(src) * K + l_chunk;
+      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(4 * wv + j);
     }
 #pragma unroll
     for (int j = 0; j < GM_B_OPS; ++j) {
@@ -191,7 +194,7 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
         wr = t.n0 + r;
       }
       wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
-      b_ptr[j] = wb + static_cast<size_t>(wr) * K + l_chunk;
+      b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(GM_B_OPS * wv + j);
     }
   };
   auto issue = [&](int step) {
@@ -222,68 +225,66 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
                                    : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - GM_NT / 2))
                   : wn * (GM_BROWS / 2) + 32 * j;
   const int a_row[2] = {wm * 64, wm * 64 + 32};
-  const int frow = lane & 31, fsel = lane >> 5, fx = lane & 7;
+  // fragment rows are 32-aligned bases + (lane % 32): (row / 2) % 8 = (lane / 2) % 8
+  const int frow = lane & 31, fsel = lane >> 5, fx = (lane >> 1) & 7;
   f32x16_t acc[2][GM_NT];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < GM_NT; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
-  for (int s = 0; s < n_steps; ++s) {
-    wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
-    lds_barrier();         // slice s visible to all waves; slice s-1 no longer read
-    if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
-    const uint16_t* As = smem + (s % GM_STAGES) * GM_STAGE_ELEMS;
-    const uint16_t* Bs = As + GM_A_ELEMS;
+  int s = 0;        // flattened step; loads run GM_STAGES-1 steps ahead, across tiles
+  for (int tile_i = 0; tile_i < n_my; ++tile_i) {
 #pragma unroll
-    for (int kk = 0; kk < GM_BK / 16; ++kk) {
-      const int slot = ((2 * kk + fsel) ^ fx) * 8;
-      bf16x8_t af[2], bfr[GM_NT];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < GM_NT; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int kt = 0; kt < nk; ++kt, ++s) {
+      wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
+      lds_barrier();       // slice s visible to all waves; slice s-1 no longer read
+      if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
+      const uint16_t* As = smem + (s % GM_STAGES) * GM_STAGE_ELEMS;
+      const uint16_t* Bs = As + GM_A_ELEMS;
+#pragma unroll
+      for (int kk = 0; kk < GM_BK / 16; ++kk) {
+        const int slot = ((2 * kk + fsel) ^ fx) * 8;
+        bf16x8_t af[2], bfr[GM_NT];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
 #pragma unroll
         for (int j = 0; j < GM_NT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < GM_NT; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
     }
-    const int tile_i = s / nk;
-    if (s - tile_i * nk == nk - 1) {
-      // epilogue: lane l, register r holds row 8 (r/4) + 4 (l/32) + r%4, column l%32
-      const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E,
-                                     dense_M, n_tiles, out_rows);
-      const int col = lane & 31;
+    // epilogue: lane l, register r holds row 8 (r/4) + 4 (l/32) + r%4, column l%32
+    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E,
+                                   dense_M, n_tiles, out_rows);
+    const int col = lane & 31;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int grow = t.row0 + a_row[i] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (grow < t.row_end) {
-            uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
-            if (UP) {
+      for (int r = 0; r < 16; ++r) {
+        const int grow = t.row0 + a_row[i] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (grow >= t.row_end) continue;
+        uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
+        if (UP) {
 #pragma unroll
-              for (int j = 0; j < GM_NT / 2; ++j) {
-                const int c = wn * (GM_BROWS / 4) + 32 * j + col;
-                const float g = acc[i][j][r], u = acc[i][j + GM_NT / 2][r];
-                if (t.n0 + c < N_out) orow[c] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
-              }
-            } else {
-#pragma unroll
-              for (int j = 0; j < GM_NT; ++j) {
-                const int c = wn * (GM_BROWS / 2) + 32 * j + col;
-                if (t.n0 + c < N_out) orow[c] = f32_to_bf16(acc[i][j][r]);
-              }
-            }
+          for (int j = 0; j < GM_NT / 2; ++j) {
+            const int c = wn * (GM_BROWS / 4) + 32 * j + col;
+            const float g = acc[i][j][r], u = acc[i][j + GM_NT / 2][r];
+            if (t.n0 + c < N_out) orow[c] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
           }
+        } else {
 #pragma unroll
-          for (int j = 0; j < GM_NT; ++j) acc[i][j][r] = 0.0f;
+          for (int j = 0; j < GM_NT; ++j) {
+            const int c = wn * (GM_BROWS / 2) + 32 * j + col;
+            if (t.n0 + c < N_out) orow[c] = f32_to_bf16(acc[i][j][r]);
+          }
         }
       }
     }

@@ -20,8 +20,14 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int RT_TE = 64;        // experts per workgroup
-constexpr int RT_TK = 32;        // K per MFMA step
-constexpr int RT_LDS = RT_TK + 8;  // padded row (bf16 elements)
+constexpr int RT_TK = 32;        // K per MFMA step: an LDS row is 64 bytes (4 chunks of 16)
+
+// Chunk c of expert row e is stored at slot c ^ ((e / 4) % 4): the 64 four-byte LDS
+// banks then see 16 distinct 16-byte groups both for a fragment read (16 rows, one
+// chunk) and for the staging writes (4 rows x 4 chunks).
+__device__ __forceinline__ int bs_index(int row, int chunk) {
+  return row * RT_TK + ((chunk ^ ((row >> 2) & 3)) << 3);
+}
 
 __device__ __forceinline__ void split3(float w, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
   const uint32_t u = __float_as_uint(w);
@@ -41,7 +47,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __rest
                                                           float* __restrict__ logits, int T, int d,
                                                           int E) {
   constexpr int NB = TM == 16 ? 1 : 4;      // 16 x 16 accumulators per wave
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][RT_TE * RT_LDS];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][RT_TE * RT_TK];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int t0 = blockIdx.x * TM, e0 = blockIdx.y * RT_TE;
 
@@ -71,7 +77,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __rest
       pk.y = t[x][2] | (uint32_t(t[x][3]) << 16);
       pk.z = t[x][4] | (uint32_t(t[x][5]) << 16);
       pk.w = t[x][6] | (uint32_t(t[x][7]) << 16);
-      *reinterpret_cast<uint4*>(&Bs[buf][x][se * RT_LDS + sk]) = pk;
+      *reinterpret_cast<uint4*>(&Bs[buf][x][bs_index(se, sk >> 3)]) = pk;
     }
   };
 
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __rest
       const int erow = (TM == 16 ? 16 * wv : 16 * b) + (lane & 15);
 #pragma unroll
       for (int x = 0; x < 3; ++x) {
-        const bf16x8_t bf = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][x][erow * RT_LDS + ak]);
+        const bf16x8_t bf = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][x][bs_index(erow, ak >> 3)]);
         acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf, acc[b], 0, 0, 0);
       }
     }
