@@ -133,7 +133,7 @@ def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: 
     from paper_2608_01784_amd import _lib
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer
     L = w.n_layers
-    lays = [MoELayer(w.T, w.d, ExpertWeights(**dws[l]), w.params, uniform_k=uniform_k) for l in range(L)]
+    lays = [MoELayer(w.T, w.d, dws[l], w.params, uniform_k=uniform_k) for l in range(L)]
     res = residuals
     hbuf = [h0, torch.empty_like(h0), torch.empty_like(h0)]
     evs = [[[ev.create() for _ in range(_lib.N_STAGE_EVENTS)] for _ in range(L)]
@@ -224,6 +224,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-uniform", action="store_true")
+    ap.add_argument("--packed-weights", action="store_true",
+                    help="pack the expert weights once (reflex_pack_*) and stream the packed layout")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -233,7 +235,7 @@ def main():
     import numpy as np
     import torch
     from paper_2608_01784_amd import _lib
-    from paper_2608_01784_amd.layer import TokenState
+    from paper_2608_01784_amd.layer import ExpertWeights, TokenState
     from synth import make_workload
     from synth.device import state_tensors, to_device
 
@@ -251,7 +253,13 @@ def main():
         dv["router_bias"] = None if w.router_bias is None else to_device(w.router_bias)
         if host["shared"] is not None:
             dv["ws_gate"], dv["ws_up"], dv["ws_down"] = (to_device(x) for x in host["shared"])
-        dws.append(dv)
+        # with --packed-weights the static weights are packed once, as at model load,
+        # and the timed forwards stream the packed copies (row-major ones dropped)
+        ew = ExpertWeights(**dv)
+        if a.packed_weights:
+            ew.pack()
+            ew.w_gate = ew.w_up = ew.w_down = None
+        dws.append(ew)
         hosts.append(host if l == 0 else None)
         if w.n_layers > 1:
             log(f"layer {l} weights resident")
@@ -288,7 +296,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "tokens": T, "hidden": d, "experts": E, "expert_ffn": f,
                    "shared_ffn": w.f_shared, "layers": L, "k_base": w.params.k_base,
-                   "k_range": [w.params.k_min, w.params.k_max], "path": "variable-K (REFLEX)"},
+                   "k_range": [w.params.k_min, w.params.k_max], "path": "variable-K (REFLEX)",
+                   "expert_weights": "packed at load" if a.packed_weights else "row-major"},
         "alloc_tflops": round(alloc_tflops, 2),
         "pct_bf16_peak": round(100 * alloc_tflops / PEAK_BF16_TFLOPS, 2),
         "pairs_per_layer": P, "avg_k": round(P / T, 4), "experts_touched": touched,

@@ -202,6 +202,24 @@ int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
                           size_t ws_bytes, void* stream);
 
 /*
+ * One-time weight pre-packing for the grouped GEMM (done once per model load, like
+ * any weight format conversion).  The packed layout stores, for every expert, N
+ * tile and 64-wide K step, the weight slice the GEMM stages in LDS as one contiguous
+ * 32 KB block, so the GEMM streams its weights sequentially from HBM.  The layout is
+ * internal to this library version; only pass buffers written by these functions.
+ *  reflex_pack_gate_up: w_gate, w_up [E, f, d] bf16 -> dst of
+ *                       reflex_packed_gate_up_size(E, f, d) bytes
+ *  reflex_pack_down:    w_down [E, d, f] bf16 -> dst of reflex_packed_down_size(E, d, f)
+ * Sizes return 0 for invalid shapes.  Errors: NULL or misaligned pointers, shapes as
+ * for reflex_grouped_swiglu.
+ */
+size_t reflex_packed_gate_up_size(int E, int f, int d);
+size_t reflex_packed_down_size(int E, int d, int f);
+int reflex_pack_gate_up(const uint16_t* w_gate, const uint16_t* w_up, int E, int f, int d,
+                        uint16_t* dst, void* stream);
+int reflex_pack_down(const uint16_t* w_down, int E, int d, int f, uint16_t* dst, void* stream);
+
+/*
  * Weighted combine (Eq. (2)): out[i] = sum over the pairs j of token i, in rank
  * order, of pair_weight[j] * y_sorted[pair_to_sorted[j]], plus shared_y[i] when
  * given; accumulated in fp32 and rounded to bf16 once.
@@ -243,6 +261,10 @@ typedef struct {
   const float    *conf_prev1, *conf_prev2;
   const int32_t  *k_in;                      /* [T] or NULL                              */
   const uint16_t *residual_a, *residual_b;   /* [T, d] bf16 added before rounding, or NULL */
+  const uint16_t *w_gate_up_packed;          /* reflex_pack_gate_up output, or NULL; when
+                                                given, w_gate and w_up may be NULL       */
+  const uint16_t *w_down_packed;             /* reflex_pack_down output, or NULL; when
+                                                given, w_down may be NULL                */
   reflex_alloc_params params;
   uint16_t *out;                             /* [T, d] bf16                              */
   int32_t  *k_out;                           /* [T] counts used, or NULL                 */

@@ -188,7 +188,7 @@ int reflex_permute(const int32_t* pair_offsets, const int32_t* pair_expert, cons
   if (ws_bytes < permute_ws_bytes(pair_capacity, E)) return REFLEX_ERR_WORKSPACE;
   if (T == 0) return REFLEX_OK;
   return launch_permute(pair_offsets, pair_expert, pairs, T, E, pair_capacity, expert_offsets,
-                        sorted_token, pair_to_sorted, ws, static_cast<hipStream_t>(stream));
+                        sorted_token, pair_to_sorted, ws, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
@@ -204,6 +204,29 @@ int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
   if (T == 0 || pair_capacity == 0) return REFLEX_OK;
   return launch_swiglu_routed(h, sorted_token, expert_offsets, w_gate, w_up, w_down, T, E, d, f,
                               pair_capacity, y_sorted, ws, static_cast<hipStream_t>(stream));
+}
+
+size_t reflex_packed_gate_up_size(int E, int f, int d) {
+  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return 0;
+  return packed_gate_up_bytes(E, f, d);
+}
+
+size_t reflex_packed_down_size(int E, int d, int f) {
+  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return 0;
+  return packed_down_bytes(E, d, f);
+}
+
+int reflex_pack_gate_up(const uint16_t* w_gate, const uint16_t* w_up, int E, int f, int d,
+                        uint16_t* dst, void* stream) {
+  RFX_TRY(check_ptrs({w_gate, w_up, dst}, 16));
+  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return REFLEX_ERR_SHAPE;
+  return launch_pack_gate_up(w_gate, w_up, E, f, d, dst, static_cast<hipStream_t>(stream));
+}
+
+int reflex_pack_down(const uint16_t* w_down, int E, int d, int f, uint16_t* dst, void* stream) {
+  RFX_TRY(check_ptrs({w_down, dst}, 16));
+  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return REFLEX_ERR_SHAPE;
+  return launch_pack_down(w_down, E, d, f, dst, static_cast<hipStream_t>(stream));
 }
 
 int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
@@ -226,7 +249,11 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || fs < 0 || (fs && !valid_f(fs)))
     return REFLEX_ERR_SHAPE;
   if (a->norm_topk != 0 && a->norm_topk != 1) return REFLEX_ERR_PARAM;
-  RFX_TRY(check_ptrs({a->h, a->w_gate, a->w_up, a->w_down, a->w_router, a->out, ws}, 16));
+  RFX_TRY(check_ptrs({a->h, a->w_router, a->out, ws}, 16));
+  if (a->w_gate_up_packed) RFX_TRY(check_ptr(a->w_gate_up_packed, 16));
+  else RFX_TRY(check_ptrs({a->w_gate, a->w_up}, 16));
+  if (a->w_down_packed) RFX_TRY(check_ptr(a->w_down_packed, 16));
+  else RFX_TRY(check_ptr(a->w_down, 16));
   for (const void* p : {static_cast<const void*>(a->residual_a), static_cast<const void*>(a->residual_b)})
     RFX_TRY(check_opt_ptr(p, 16));
   for (const void* p : {static_cast<const void*>(a->router_bias), static_cast<const void*>(a->k_in),
@@ -282,8 +309,8 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
       RFX_TRY(launch_fill_i32(kb, a->uniform_k, T, s));
     } else {
       RFX_TRY(launch_budget(a->block_idx, a->masked, a->hist_len, a->conf_prev1, a->conf_prev2,
-                            a->seq_offsets, a->active_block, a->B, T, a->params, kb,
-                            static_cast<int32_t*>(at(L.scalar)), nullptr, s));
+                            a->seq_offsets, a->active_block, a->B, T, a->params, kb, nullptr,
+                            nullptr, s));
     }
     k = kb;
   }
@@ -292,14 +319,14 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   RFX_TRY(launch_count_scan(k, T, kcap, pair_offsets, a->pairs_out, s));
   RFX_TRY(launch_topk(logits, k, T, E, kcap, a->norm_topk, pair_offsets, pair_expert, pair_weight, s));
   RFX_TRY(mark(3));
+  // the permutation's scan also writes the GEMM tile plan at the head of gws
   RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
-                         sorted_token, pair_to_sorted, at(L.perm), s));
-  RFX_TRY(launch_swiglu_plan(expert_offsets, E, gws, s));
+                         sorted_token, pair_to_sorted, at(L.perm), static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(4));
-  RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up, T, E, d, f, cap,
-                           gws, s));
+  RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up,
+                           a->w_gate_up_packed, T, E, d, f, cap, gws, s));
   RFX_TRY(mark(5));
-  RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, E, d, f, cap, y, gws, s));
+  RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, a->w_down_packed, E, d, f, cap, y, gws, s));
   RFX_TRY(mark(6));
   const uint16_t* shared_y = nullptr;
   if (fs) {

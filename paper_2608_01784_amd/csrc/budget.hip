@@ -82,29 +82,53 @@ __global__ __launch_bounds__(BG_THREADS) void budget_kernel(
   const int k_cur = p.k_base + p.delta_role;
   const int tid = threadIdx.x;
 
-  auto is_cand = [&](int i) {
-    return masked[i] != 0 && block_idx[i] == a && hist_len[i] >= 1;
+  // own tokens of one slice: candidate flag (masked, in the active block, with
+  // confidence history), its ranking key, and the RRB count H(|b - a|) (Eq. (5))
+  double key[BG_PER_THREAD];
+  int rank[BG_PER_THREAD], kr[BG_PER_THREAD];
+  bool cand[BG_PER_THREAD];
+  auto load_slice = [&](int c0) {
+#pragma unroll
+    for (int r = 0; r < BG_PER_THREAD; ++r) {
+      const int i = c0 + r * BG_THREADS + tid;
+      cand[r] = false;
+      key[r] = 0.0;
+      rank[r] = 0;
+      kr[r] = 0;
+      if (i < hi) {
+        // every field is loaded up front (one round of memory latency)
+        const int b = block_idx[i];
+        const bool msk = masked[i] != 0;
+        const int hl = hist_len[i];
+        const float x1 = c1[i], x2 = c2[i];
+        const bool in_j = msk && b == a;
+        const int dist = b > a ? b - a : a - b;
+        kr[r] = in_j ? k_cur
+                     : (dist <= 1 ? p.k_base + p.delta_role
+                                  : (dist == 2 ? p.k_base : p.k_base - p.delta_role));
+        cand[r] = in_j && hl >= 1;
+        if (cand[r]) key[r] = rank_key(p, x1, x2, hl);
+      }
+    }
   };
 
   // m = |J'|, the number of ranked tokens of this sequence
+  const bool single = hi - lo <= BG_CHUNK;      // uniform: one slice holds the sequence
   int mine = 0;
-  for (int i = lo + tid; i < hi; i += BG_THREADS) mine += is_cand(i) ? 1 : 0;
+  if (single) {
+    load_slice(lo);
+#pragma unroll
+    for (int r = 0; r < BG_PER_THREAD; ++r) mine += cand[r] ? 1 : 0;
+  } else {
+    for (int i = lo + tid; i < hi; i += BG_THREADS)
+      mine += (masked[i] != 0 && block_idx[i] == a && hist_len[i] >= 1) ? 1 : 0;
+  }
   const int m = block_sum(mine, s_red);
   const int n_q = static_cast<int>(floor(p.q * static_cast<double>(m)));
 
   int total = 0;
   for (int c0 = lo; c0 < hi; c0 += BG_CHUNK) {
-    // own tokens of this slice and their keys
-    double key[BG_PER_THREAD];
-    int rank[BG_PER_THREAD];
-    bool cand[BG_PER_THREAD];
-#pragma unroll
-    for (int r = 0; r < BG_PER_THREAD; ++r) {
-      const int i = c0 + r * BG_THREADS + tid;
-      cand[r] = i < hi && is_cand(i);
-      key[r] = cand[r] ? rank_key(p, c1[i], c2[i], hist_len[i]) : 0.0;
-      rank[r] = 0;
-    }
+    if (!single) load_slice(c0);
     if (m > 0) {
       for (int d0 = lo; d0 < hi; d0 += BG_CHUNK) {
         // stage the candidates of slice d0 (slot order is irrelevant to the count)
@@ -113,8 +137,16 @@ __global__ __launch_bounds__(BG_THREADS) void budget_kernel(
 #pragma unroll
         for (int r = 0; r < BG_PER_THREAD; ++r) {
           const int j = d0 + r * BG_THREADS + tid;
-          if (j < hi && is_cand(j)) {
-            const double kj = (d0 == c0) ? key[r] : rank_key(p, c1[j], c2[j], hist_len[j]);
+          bool cj;
+          double kj;
+          if (d0 == c0) {
+            cj = cand[r];
+            kj = key[r];
+          } else {
+            cj = j < hi && masked[j] != 0 && block_idx[j] == a && hist_len[j] >= 1;
+            kj = cj ? rank_key(p, c1[j], c2[j], hist_len[j]) : 0.0;
+          }
+          if (cj) {
             const int slot = atomicAdd(&s_cnt, 1);
             s_key[slot] = kj;
             s_idx[slot] = j;
@@ -140,11 +172,8 @@ __global__ __launch_bounds__(BG_THREADS) void budget_kernel(
     for (int r = 0; r < BG_PER_THREAD; ++r) {
       const int i = c0 + r * BG_THREADS + tid;
       if (i >= hi) continue;
-      const int b = block_idx[i];
-      const int dist = b > a ? b - a : a - b;
-      int k = dist <= 1 ? p.k_base + p.delta_role : (dist == 2 ? p.k_base : p.k_base - p.delta_role);
-      if (masked[i] != 0 && b == a) k = k_cur;
-      if (cand[r]) {
+      int k = kr[r];
+      if (cand[r]) {      // Eq. (9): high / middle / low group by rank
         if (rank[r] < n_q) k = k_cur + p.delta_cur;
         else if (rank[r] >= m - n_q) k = k_cur - p.delta_cur;
       }
@@ -154,8 +183,10 @@ __global__ __launch_bounds__(BG_THREADS) void budget_kernel(
       if (fps_out) fps_out[i] = cand[r] ? key[r] : __longlong_as_double(0x7ff8000000000000ll);
     }
   }
-  total = block_sum(total, s_red);
-  if (tid == 0 && total != 0) atomicAdd(pairs_out, total);
+  if (pairs_out) {        // uniform
+    total = block_sum(total, s_red);
+    if (tid == 0 && total != 0) atomicAdd(pairs_out, total);
+  }
 }
 
 __global__ void fill_i32_kernel(int32_t* dst, int32_t v, int n) {
@@ -221,8 +252,10 @@ int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t*
   p.q = prm.q; p.theta = prm.theta; p.w = prm.w_cf; p.v_ref = prm.v_ref; p.tau = prm.tau;
   p.k_base = prm.k_base; p.delta_role = prm.delta_role; p.delta_cur = prm.delta_cur;
   p.k_min = prm.k_min; p.k_max = prm.k_max; p.signal = prm.signal;
-  int rc = launch_fill_i32(pairs_out, 0, 1, s);
-  if (rc != REFLEX_OK) return rc;
+  if (pairs_out != nullptr) {
+    const int rc = launch_fill_i32(pairs_out, 0, 1, s);
+    if (rc != REFLEX_OK) return rc;
+  }
   hipLaunchKernelGGL(budget_kernel, dim3(B), dim3(BG_THREADS), 0, s, block_idx, masked, hist_len,
                      c1, c2, seq_offsets, active_block, T, p, k_out, pairs_out, fps_out);
   return launch_status();

@@ -12,6 +12,7 @@
 namespace rfx {
 
 constexpr int kWave = 64;
+constexpr int kGemmBM = 128;   // M tile (rows) of the grouped SwiGLU GEMM
 
 // ---- bf16 <-> fp32 ------------------------------------------------------------------
 RFX_DEVICE float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
@@ -84,6 +85,7 @@ namespace rfx {
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
                   int d, int E, hipStream_t s);
 
+// pairs_out may be NULL (the fused forward takes P from the count scan instead).
 int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
                   const float* c1, const float* c2, const int32_t* seq_offsets,
                   const int32_t* active_block, int B, int T, const reflex_alloc_params& p,
@@ -99,9 +101,11 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
                 hipStream_t s);
 
 size_t permute_ws_bytes(int pair_capacity, int E);
+// gemm_tile_off (nullable): also write the grouped GEMM's per-expert M-tile prefix.
 int launch_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
                    int T, int E, int pair_capacity, int32_t* expert_offsets,
-                   int32_t* sorted_token, int32_t* pair_to_sorted, void* ws, hipStream_t s);
+                   int32_t* sorted_token, int32_t* pair_to_sorted, void* ws,
+                   int32_t* gemm_tile_off, hipStream_t s);
 
 size_t swiglu_ws_bytes(int pair_capacity, int E, int f);
 // Routed experts: rows grouped by expert_offsets, inputs gathered through sorted_token.
@@ -111,11 +115,18 @@ int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
                          uint16_t* y_sorted, void* ws, hipStream_t s);
 // The same in three steps: per-expert M-tile plan, gate/up GEMM, down GEMM.
 int launch_swiglu_plan(const int32_t* expert_offsets, int E, void* ws, hipStream_t s);
+// w_packed (nullable): weights in the packed layout of launch_pack_*; used instead of
+// the row-major weights when given.
 int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32_t* expert_offsets,
-                     const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
-                     void* ws, hipStream_t s);
-int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
-                       int cap, uint16_t* y_sorted, void* ws, hipStream_t s);
+                     const uint16_t* wg, const uint16_t* wu, const uint16_t* w_packed, int T, int E,
+                     int d, int f, int cap, void* ws, hipStream_t s);
+int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, const uint16_t* w_packed,
+                       int E, int d, int f, int cap, uint16_t* y_sorted, void* ws, hipStream_t s);
+size_t packed_gate_up_bytes(int E, int f, int d);
+size_t packed_down_bytes(int E, int d, int f);
+int launch_pack_gate_up(const uint16_t* wg, const uint16_t* wu, int E, int f, int d, uint16_t* dst,
+                        hipStream_t s);
+int launch_pack_down(const uint16_t* wd, int E, int d, int f, uint16_t* dst, hipStream_t s);
 // One dense expert over rows 0..M-1 of x (the always-on shared expert).
 size_t swiglu_dense_ws_bytes(int M, int f);
 int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* wu,

@@ -45,20 +45,32 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 #ifndef RFX_GEMM_STAGES
 #define RFX_GEMM_STAGES 3
 #endif
-constexpr int GM_BM = 128;
-constexpr int GM_BK = 64;
+constexpr int GM_BM = kGemmBM;
+#ifndef RFX_GEMM_BK
+#define RFX_GEMM_BK 64
+#endif
+constexpr int GM_BK = RFX_GEMM_BK;         // K per pipeline step: 64 or 32
 constexpr int GM_THREADS = 256;
 constexpr int GM_BROWS = RFX_GEMM_BROWS;   // weight (B) rows per tile: 128 or 256
 constexpr int GM_UP_BN = GM_BROWS / 2;     // activation columns per up-GEMM tile (gate + up rows)
 constexpr int GM_DOWN_BN = GM_BROWS;       // output columns per down-GEMM tile
-constexpr int GM_A_ELEMS = GM_BM * GM_BK;      // A slice: 128 rows x 64
+constexpr int GM_A_ELEMS = GM_BM * GM_BK;      // A slice: 128 rows x BK
 constexpr int GM_B_ELEMS = GM_BROWS * GM_BK;   // B slice
 constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
 constexpr int GM_STAGES = RFX_GEMM_STAGES;
 constexpr int GM_XCDS = 8;
 constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per wave
-constexpr int GM_B_OPS = GM_BROWS / 32;    // 8-row DMA ops per wave for B
-constexpr int GM_OPS = 4 + GM_B_OPS;       // vector-memory ops per thread per step
+// LDS rows are BK bf16 = CH chunks of 16 bytes; one DMA op (a wave, 64 lanes x 16
+// bytes = 1 KB) fills ROWS_PER_OP whole rows.  Chunk c of row r sits in slot
+// c ^ ((r / RG) % CH), RG = 16 / CH: the 16 rows one 16-lane group reads cover all
+// 64 four-byte banks exactly once.
+constexpr int GM_CH = GM_BK / 8;
+constexpr int GM_ROWS_PER_OP = 64 / GM_CH;
+constexpr int GM_RG = 16 / GM_CH;
+constexpr int GM_A_OPS = GM_BM / GM_ROWS_PER_OP / 4;      // DMA ops per wave per step for A
+constexpr int GM_B_OPS = GM_BROWS / GM_ROWS_PER_OP / 4;   // ... and for B
+constexpr int GM_OPS = GM_A_OPS + GM_B_OPS;               // vector-memory ops per thread per step
+static_assert(GM_BK == 32 || GM_BK == 64, "BK");
 
 struct Tile {
   int expert, row0, row_end, n0;
@@ -135,8 +147,10 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ expert_offsets, int E,
     int dense_M, const uint16_t* __restrict__ w0,   // UP: W_gate; DOWN: W_down
     const uint16_t* __restrict__ w1,                // UP: W_up
-    size_t w_expert_stride, int K, int N_out, int x_rows, int out_rows,
+    size_t w_expert_stride, int K, int N_out, int x_rows, int out_rows, int packed,
     uint16_t* __restrict__ out) {
+  // packed != 0: w0 holds the weights as per-(expert, N tile, K step) slices, each the
+  // contiguous 32 KB LDS image of the B operand (see pack_weights_kernel)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = (N_out + BN - 1) / BN;     // the last N tile may be partial
@@ -162,8 +176,11 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
   // op q of a wave fills rows R0 = 8 q' .. 8 q' + 7 (q' the op's global 8-row index);
   // lane L writes row r = R0 + L / 8, slot L % 8, which must hold logical chunk
   // c = (L % 8) ^ ((r / 2) % 8) = (L % 8) ^ (4 (q' % 2) + L / 16).
-  auto lane_chunk = [&](int q) { return ((lane & 7) ^ (((q & 1) << 2) | (lane >> 4))) * 8; };
-  const uint16_t* a_ptr[4];
+  auto lane_row = [&](int q) { return q * GM_ROWS_PER_OP + lane / GM_CH; };
+  auto lane_chunk = [&](int q) {
+    return ((lane % GM_CH) ^ ((lane_row(q) / GM_RG) % GM_CH)) * 8;
+  };
+  const uint16_t* a_ptr[GM_A_OPS];
   const uint16_t* b_ptr[GM_B_OPS];
   int ld_tile = -1;
   auto setup_loader = [&](int tile_i) {
@@ -171,19 +188,26 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
                                    n_tiles, out_rows);
     const int rows_valid = t.row_end - t.row0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = (4 * wv + j) * 8 + (lane >> 3);
+    for (int j = 0; j < GM_A_OPS; ++j) {
+      const int r = lane_row(GM_A_OPS * wv + j);
       int src = t.row0 + (r < rows_valid ? r : 0);     // rows past the expert reuse row0
       if (rows_valid <= 0) src = 0;
       if (UP && gather != nullptr) {
         src = gather[src];
         src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
       }
-      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(4 * wv + j);
+      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(GM_A_OPS * wv + j);
+    }
+    if (packed) {
+      const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
+#pragma unroll
+      for (int j = 0; j < GM_B_OPS; ++j)
+        b_ptr[j] = w0 + slice0 * GM_B_ELEMS + (GM_B_OPS * wv + j) * 512 + lane * 8;
+      return;
     }
 #pragma unroll
     for (int j = 0; j < GM_B_OPS; ++j) {
-      const int r = (GM_B_OPS * wv + j) * 8 + (lane >> 3);
+      const int r = lane_row(GM_B_OPS * wv + j);
       const uint16_t* wb;
       int wr;
       if (UP) {     // rows [0, BROWS/2): gate rows n0 + r; the rest: up rows n0 + r - BROWS/2
@@ -206,12 +230,13 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
     uint16_t* As = smem + (step % GM_STAGES) * GM_STAGE_ELEMS;
     uint16_t* Bs = As + GM_A_ELEMS;
     const int k0 = kt * GM_BK;
+    const size_t kb = packed ? static_cast<size_t>(kt) * GM_B_ELEMS : static_cast<size_t>(k0);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      __builtin_amdgcn_global_load_lds(a_ptr[j] + k0, As + (4 * wv + j) * 512, 16, 0, 0);
+    for (int j = 0; j < GM_A_OPS; ++j)
+      __builtin_amdgcn_global_load_lds(a_ptr[j] + k0, As + (GM_A_OPS * wv + j) * 512, 16, 0, 0);
 #pragma unroll
     for (int j = 0; j < GM_B_OPS; ++j)
-      __builtin_amdgcn_global_load_lds(b_ptr[j] + k0, Bs + (GM_B_OPS * wv + j) * 512, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(b_ptr[j] + kb, Bs + (GM_B_OPS * wv + j) * 512, 16, 0, 0);
   };
 
   // ---- multiply ----
@@ -226,7 +251,7 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
                   : wn * (GM_BROWS / 2) + 32 * j;
   const int a_row[2] = {wm * 64, wm * 64 + 32};
   // fragment rows are 32-aligned bases + (lane % 32): (row / 2) % 8 = (lane / 2) % 8
-  const int frow = lane & 31, fsel = lane >> 5, fx = (lane >> 1) & 7;
+  const int frow = lane & 31, fsel = lane >> 5, fx = (frow / GM_RG) % GM_CH;
   f32x16_t acc[2][GM_NT];
 
   for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
@@ -312,6 +337,47 @@ __global__ __launch_bounds__(256) void tile_plan_kernel(const int32_t* __restric
   }
 }
 
+// Packed weight layout: for expert e, N tile n and K step kt, a contiguous slice of
+// GM_B_ELEMS bf16 that is byte for byte the LDS image the GEMM loader builds for
+// the B operand: 8-row groups q of 1 KB, lane L of a group holding row 8q + L/8,
+// logical chunk (L % 8) ^ (4 (q % 2) + L / 16).  UP interleaves per tile the
+// BROWS/2 gate rows and the matching up rows; rows past N repeat row N-1.  A
+// workgroup then streams whole 32 KB slices in order.
+template <bool UP>
+__global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* __restrict__ w0,
+                                                           const uint16_t* __restrict__ w1,
+                                                           int E, int N, int K,
+                                                           uint16_t* __restrict__ dst) {
+  constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
+  const int n_tiles = (N + BN - 1) / BN, nk = K / GM_BK;
+  const size_t units = static_cast<size_t>(E) * n_tiles * nk * (GM_B_ELEMS / 8);
+  for (size_t u = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; u < units;
+       u += static_cast<size_t>(gridDim.x) * 256) {
+    const int within = static_cast<int>(u % (GM_B_ELEMS / 8));
+    size_t slice = u / (GM_B_ELEMS / 8);
+    const int kt = static_cast<int>(slice % nk);
+    slice /= nk;
+    const int nt = static_cast<int>(slice % n_tiles);
+    const int e = static_cast<int>(slice / n_tiles);
+    const int q = within >> 6, L = within & 63;
+    const int r = q * GM_ROWS_PER_OP + L / GM_CH;
+    const int c = (L % GM_CH) ^ ((r / GM_RG) % GM_CH);
+    const uint16_t* src;
+    int row;
+    if (UP) {
+      src = r < GM_BROWS / 2 ? w0 : w1;
+      row = nt * BN + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
+    } else {
+      src = w0;
+      row = nt * BN + r;
+    }
+    row = row < N ? row : N - 1;
+    const uint4 v = *reinterpret_cast<const uint4*>(
+        src + (static_cast<size_t>(e) * N + row) * K + kt * GM_BK + c * 8);
+    *reinterpret_cast<uint4*>(dst + u * 8) = v;
+  }
+}
+
 constexpr size_t kGemmLds = size_t(GM_STAGES) * GM_STAGE_ELEMS * sizeof(uint16_t);
 
 // One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
@@ -332,7 +398,7 @@ int persistent_grid() {
 template <bool UP>
 int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_off,
                 const int32_t* eo, int E, int dense_M, const uint16_t* w0, const uint16_t* w1,
-                size_t stride, int K, int N, int x_rows, int out_rows, uint16_t* out,
+                size_t stride, int K, int N, int x_rows, int out_rows, int packed, uint16_t* out,
                 hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
@@ -344,7 +410,7 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
   }
   hipLaunchKernelGGL(swiglu_gemm_kernel<UP>, dim3(persistent_grid()), dim3(GM_THREADS), kGemmLds, s,
                      x, gather, tile_off, eo, E, dense_M, w0, w1, stride, K, N, x_rows, out_rows,
-                     out);
+                     packed, out);
   return launch_status();
 }
 
@@ -370,19 +436,43 @@ static uint16_t* routed_act(void* ws, int E) {
 }
 
 int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32_t* expert_offsets,
-                     const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
-                     void* ws, hipStream_t s) {
+                     const uint16_t* wg, const uint16_t* wu, const uint16_t* w_packed, int T, int E,
+                     int d, int f, int cap, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
-                           wg, wu, static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
+                           w_packed ? w_packed : wg, wu, static_cast<size_t>(f) * d, d, f, T, cap,
+                           w_packed != nullptr, routed_act(ws, E), s);
 }
 
-int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
-                       int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
+int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, const uint16_t* w_packed,
+                       int E, int d, int f, int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
-                            expert_offsets, E, -1, wd, nullptr, static_cast<size_t>(d) * f, f, d,
-                            cap, cap, y_sorted, s);
+                            expert_offsets, E, -1, w_packed ? w_packed : wd, nullptr,
+                            static_cast<size_t>(d) * f, f, d, cap, cap, w_packed != nullptr,
+                            y_sorted, s);
+}
+
+size_t packed_gate_up_bytes(int E, int f, int d) {
+  return static_cast<size_t>(E) * ((f + GM_UP_BN - 1) / GM_UP_BN) * (d / GM_BK) * GM_B_ELEMS *
+         sizeof(uint16_t);
+}
+
+size_t packed_down_bytes(int E, int d, int f) {
+  return static_cast<size_t>(E) * ((d + GM_DOWN_BN - 1) / GM_DOWN_BN) * (f / GM_BK) * GM_B_ELEMS *
+         sizeof(uint16_t);
+}
+
+int launch_pack_gate_up(const uint16_t* wg, const uint16_t* wu, int E, int f, int d, uint16_t* dst,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(pack_weights_kernel<true>, dim3(2048), dim3(256), 0, s, wg, wu, E, f, d, dst);
+  return launch_status();
+}
+
+int launch_pack_down(const uint16_t* wd, int E, int d, int f, uint16_t* dst, hipStream_t s) {
+  hipLaunchKernelGGL(pack_weights_kernel<false>, dim3(2048), dim3(256), 0, s, wd, nullptr, E, d, f,
+                     dst);
+  return launch_status();
 }
 
 int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
@@ -391,8 +481,10 @@ int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
                          uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
   int rc = launch_swiglu_plan(expert_offsets, E, ws, s);
-  if (rc == REFLEX_OK) rc = launch_swiglu_up(h, sorted_token, expert_offsets, wg, wu, T, E, d, f, cap, ws, s);
-  if (rc == REFLEX_OK) rc = launch_swiglu_down(expert_offsets, wd, E, d, f, cap, y_sorted, ws, s);
+  if (rc == REFLEX_OK)
+    rc = launch_swiglu_up(h, sorted_token, expert_offsets, wg, wu, nullptr, T, E, d, f, cap, ws, s);
+  if (rc == REFLEX_OK)
+    rc = launch_swiglu_down(expert_offsets, wd, nullptr, E, d, f, cap, y_sorted, ws, s);
   return rc;
 }
 
@@ -401,9 +493,9 @@ int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* w
                         hipStream_t s) {
   if (M <= 0) return REFLEX_OK;
   uint16_t* act = static_cast<uint16_t*>(ws);
-  int rc = launch_gemm<true>(x, nullptr, nullptr, nullptr, 1, M, wg, wu, 0, d, f, M, M, act, s);
+  int rc = launch_gemm<true>(x, nullptr, nullptr, nullptr, 1, M, wg, wu, 0, d, f, M, M, 0, act, s);
   if (rc == REFLEX_OK)
-    rc = launch_gemm<false>(act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, 0, f, d, M, M, y, s);
+    rc = launch_gemm<false>(act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, 0, f, d, M, M, 0, y, s);
   return rc;
 }
 

@@ -68,17 +68,20 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
 
 // ------------------------------------------------------------------------------------
 // Permutation: stable counting sort of the token-major pair list by expert.
-//   1. per 4096-pair tile, an LDS histogram over experts
+//   1. per 1024-pair tile, an LDS histogram over experts
 //   2. one workgroup turns the [tile][expert] counts into start rows, expert-major
-//      then tile-minor, and writes expert_offsets
-//   3. per tile, 256-pair steps: each wave finds the lanes holding the same expert
-//      with eight ballots (one per bit of the expert id), ranks them by lane, and
-//      the waves of the step are ordered through LDS counts, so rows follow pair
-//      order within each expert (i.e. token order).
+//      then tile-minor, writes expert_offsets and (optionally) the grouped GEMM's
+//      per-expert M-tile prefix
+//   3. per tile: an LDS table of each pair's owning token, then 256-pair steps in
+//      which each wave finds the lanes holding the same expert with eight ballots
+//      (one per bit of the expert id) and ranks them by lane; the waves of a step
+//      are ordered through LDS counts, so rows follow pair order within each expert
+//      (i.e. token order).
 // ------------------------------------------------------------------------------------
-constexpr int PM_TILE = 4096;
+constexpr int PM_TILE = 1024;
 constexpr int PM_THREADS = 256;
 constexpr int PM_STEPS = PM_TILE / PM_THREADS;
+constexpr int PM_SCAN_THREADS = 1024;
 
 __device__ __forceinline__ int pair_count(const int32_t* pairs, int cap) {
   int P = *pairs;
@@ -95,6 +98,7 @@ __global__ __launch_bounds__(PM_THREADS) void perm_hist_kernel(const int32_t* __
   for (int e = tid; e < E; e += PM_THREADS) cnt[e] = 0;
   __syncthreads();
   const int begin = t * PM_TILE;
+#pragma unroll
   for (int j = 0; j < PM_STEPS; ++j) {
     const int p = begin + j * PM_THREADS + tid;
     if (p < P) {
@@ -107,24 +111,59 @@ __global__ __launch_bounds__(PM_THREADS) void perm_hist_kernel(const int32_t* __
   for (int e = tid; e < E; e += PM_THREADS) hist[static_cast<size_t>(t) * E + e] = cnt[e];
 }
 
-__global__ __launch_bounds__(PM_THREADS) void perm_scan_kernel(int32_t* __restrict__ hist,
-                                                               int n_tiles, int E,
-                                                               int32_t* __restrict__ expert_offsets) {
-  __shared__ int s_wave[PM_THREADS / kWave];
-  const int e = threadIdx.x, lane = e & 63, wv = e >> 6;
+// 1024 threads: group q = tid / 256 owns a contiguous quarter of the tiles, thread
+// e = tid % 256 one expert.  Group sums give expert totals; group 0 scans them into
+// expert_offsets (and the grouped GEMM's per-expert M-tile prefix); each group then
+// rewrites its tiles' counts as start rows (expert base + earlier groups + earlier
+// tiles of the group).
+__global__ __launch_bounds__(PM_SCAN_THREADS) void perm_scan_kernel(
+    int32_t* __restrict__ hist, int n_tiles, int E, int32_t* __restrict__ expert_offsets,
+    int32_t* __restrict__ gemm_tile_off) {
+  __shared__ int s_part[4][REFLEX_MAX_EXPERTS];
+  __shared__ int s_base[REFLEX_MAX_EXPERTS];
+  __shared__ int s_wave[8];
+  const int tid = threadIdx.x, q = tid >> 8, e = tid & 255, lane = tid & 63, wv = tid >> 6;
+  const int per = (n_tiles + 3) / 4;
+  const int tb = q * per, te = min(n_tiles, tb + per);
   int n = 0;
   if (e < E)
-    for (int t = 0; t < n_tiles; ++t) n += hist[static_cast<size_t>(t) * E + e];
-  const int incl = wave_inclusive_scan_i32(n, lane);
-  if (lane == 63) s_wave[wv] = incl;
+    for (int t = tb; t < te; ++t) n += hist[static_cast<size_t>(t) * E + e];
+  s_part[q][e] = n;
   __syncthreads();
-  int base = incl - n;
-  for (int x = 0; x < wv; ++x) base += s_wave[x];
+  int tot = 0, incl = 0, tiles = 0, tincl = 0;
+  if (q == 0) {            // waves 0..3
+    tot = e < E ? s_part[0][e] + s_part[1][e] + s_part[2][e] + s_part[3][e] : 0;
+    tiles = (tot + kGemmBM - 1) / kGemmBM;
+    incl = wave_inclusive_scan_i32(tot, lane);
+    tincl = wave_inclusive_scan_i32(tiles, lane);
+    if (lane == 63) {
+      s_wave[wv] = incl;
+      s_wave[4 + wv] = tincl;
+    }
+  }
+  __syncthreads();
+  if (q == 0) {
+    int off = 0, toff = 0;
+    for (int x = 0; x < wv; ++x) {
+      off += s_wave[x];
+      toff += s_wave[4 + x];
+    }
+    const int base = off + incl - tot;
+    s_base[e] = base;
+    if (e < E) {
+      expert_offsets[e] = base;
+      if (e == E - 1) expert_offsets[E] = base + tot;
+      if (gemm_tile_off != nullptr) {
+        gemm_tile_off[e] = toff + tincl - tiles;
+        if (e == E - 1) gemm_tile_off[E] = toff + tincl;
+      }
+    }
+  }
+  __syncthreads();
   if (e < E) {
-    expert_offsets[e] = base;
-    if (e == E - 1) expert_offsets[E] = base + n;
-    int run = base;
-    for (int t = 0; t < n_tiles; ++t) {
+    int run = s_base[e];
+    for (int qq = 0; qq < q; ++qq) run += s_part[qq][e];
+    for (int t = tb; t < te; ++t) {
       const size_t x = static_cast<size_t>(t) * E + e;
       const int c = hist[x];
       hist[x] = run;
@@ -148,32 +187,35 @@ __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
     int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted) {
   __shared__ int run[REFLEX_MAX_EXPERTS];
   __shared__ int wcnt[PM_THREADS / kWave][REFLEX_MAX_EXPERTS];
+  __shared__ int owner[PM_TILE];
   __shared__ int s_tok[2];
   const int P = pair_count(pairs, cap);
   const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int begin = t * PM_TILE;
   if (begin >= P) return;
+  const int end = min(begin + PM_TILE, P);
   for (int e = tid; e < E; e += PM_THREADS) {
     run[e] = start[static_cast<size_t>(t) * E + e];
 #pragma unroll
     for (int w = 0; w < PM_THREADS / kWave; ++w) wcnt[w][e] = 0;
   }
-  if (tid == 0) {
-    const int last = (begin + PM_TILE < P ? begin + PM_TILE : P) - 1;
-    s_tok[0] = owner_token(pair_offsets, 0, T - 1, begin);
-    s_tok[1] = owner_token(pair_offsets, 0, T - 1, last);
+  if (tid < 2) s_tok[tid] = owner_token(pair_offsets, 0, T - 1, tid == 0 ? begin : end - 1);
+  __syncthreads();
+  // owning token of every pair of the tile
+  for (int i = s_tok[0] + tid; i <= s_tok[1]; i += PM_THREADS) {
+    const int p0 = max(pair_offsets[i], begin), p1 = min(pair_offsets[i + 1], end);
+    for (int p = p0; p < p1; ++p) owner[p - begin] = i;
   }
   __syncthreads();
-  const int tok_lo = s_tok[0], tok_hi = s_tok[1];
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   for (int j = 0; j < PM_STEPS; ++j) {
     const int p = begin + j * PM_THREADS + tid;
-    const bool valid = p < P;
+    const bool valid = p < end;
     int e = 0, tok = 0;
     if (valid) {
       e = pair_expert[p];
       e = e < 0 ? 0 : (e >= E ? E - 1 : e);
-      tok = owner_token(pair_offsets, tok_lo, tok_hi, p);
+      tok = owner[p - begin];
     }
     uint64_t same = __ballot(valid);
 #pragma unroll
@@ -202,7 +244,7 @@ __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
       run[x] += add;
     }
     __syncthreads();
-    if (begin + (j + 1) * PM_THREADS >= P) break;   // uniform across the workgroup
+    if (begin + (j + 1) * PM_THREADS >= end) break;   // uniform across the workgroup
   }
 }
 
@@ -224,13 +266,13 @@ size_t permute_ws_bytes(int pair_capacity, int E) {
 
 int launch_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
                    int T, int E, int cap, int32_t* expert_offsets, int32_t* sorted_token,
-                   int32_t* pair_to_sorted, void* ws, hipStream_t s) {
+                   int32_t* pair_to_sorted, void* ws, int32_t* gemm_tile_off, hipStream_t s) {
   const int n_tiles = perm_tiles(cap);
   int32_t* hist = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(perm_hist_kernel, dim3(n_tiles), dim3(PM_THREADS), 0, s, pair_expert, pairs,
                      cap, E, hist);
-  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(PM_THREADS), 0, s, hist, n_tiles, E,
-                     expert_offsets);
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(PM_SCAN_THREADS), 0, s, hist, n_tiles, E,
+                     expert_offsets, gemm_tile_off);
   hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(PM_THREADS), 0, s, pair_offsets,
                      pair_expert, pairs, T, cap, E, hist, sorted_token, pair_to_sorted);
   return launch_status();

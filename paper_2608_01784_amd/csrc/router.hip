@@ -6,11 +6,17 @@
 // product of a bf16 h with a bf16 term is exact in fp32, so three
 // v_mfma_f32_16x16x32_bf16 per K step give h . w with fp32 accumulation only.
 //
-// Workgroup tile: TM tokens x 64 experts, 4 waves.  The 64 x 32 slice of W_r for
-// each K step is loaded once per workgroup, split, and staged in LDS (double
-// buffered); h fragments are loaded straight from global memory.
-//   TM = 16: wave w computes the 16 tokens x experts 16w..16w+15   (small T)
-//   TM = 64: wave w computes tokens 16w..16w+15 x all 64 experts   (large T)
+// The contraction is short (E x d per token) and the layer's token count can be
+// small, so parallelism comes from splitting K: a workgroup owns TM tokens x 16 EB
+// experts and its KSPLIT waves each take 1/KSPLIT of d.  Every lane loads exactly the
+// operand fragments it feeds to the MFMA (2 x 8 bytes of h, 4 x 2 x 16 bytes of W_r
+// per 32-wide K step) and splits its own weights in registers, so the K loop has no
+// LDS traffic and no barrier; a wave issues the loads of PF steps before using any.
+// The partial tiles are summed through LDS in a fixed wave order, so the result is
+// deterministic.
+//   TM = 16, EB = 1, KSPLIT = 16 (small T): one 16 x 16 block per wave
+//   TM = 64, EB = 4, KSPLIT = 4  (large T): 4 token blocks x 4 expert blocks per
+//                                           wave (each W_r fragment feeds 4 blocks)
 #include "common.h"
 
 namespace rfx {
@@ -19,117 +25,122 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int RT_TE = 64;        // experts per workgroup
-constexpr int RT_TK = 32;        // K per MFMA step: an LDS row is 64 bytes (4 chunks of 16)
+constexpr int RT_TK = 32;        // K per MFMA step
 
-// Chunk c of expert row e is stored at slot c ^ ((e / 4) % 4): the 64 four-byte LDS
-// banks then see 16 distinct 16-byte groups both for a fragment read (16 rows, one
-// chunk) and for the staging writes (4 rows x 4 chunks).
-__device__ __forceinline__ int bs_index(int row, int chunk) {
-  return row * RT_TK + ((chunk ^ ((row >> 2) & 3)) << 3);
+__device__ __forceinline__ void split3x8(const float4& lo4, const float4& hi4, bf16x8_t& t0,
+                                         bf16x8_t& t1, bf16x8_t& t2) {
+  const float v[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t uh = __float_as_uint(v[j]) & 0xffff0000u;
+    const float r1 = v[j] - __uint_as_float(uh);
+    const uint32_t um = __float_as_uint(r1) & 0xffff0000u;
+    const float r2 = r1 - __uint_as_float(um);
+    t0[j] = __builtin_bit_cast(__bf16, static_cast<uint16_t>(uh >> 16));
+    t1[j] = __builtin_bit_cast(__bf16, static_cast<uint16_t>(um >> 16));
+    t2[j] = __builtin_bit_cast(__bf16, static_cast<uint16_t>(__float_as_uint(r2) >> 16));
+  }
 }
 
-__device__ __forceinline__ void split3(float w, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
-  const uint32_t u = __float_as_uint(w);
-  const uint32_t uh = u & 0xffff0000u;
-  const float r1 = w - __uint_as_float(uh);
-  const uint32_t um = __float_as_uint(r1) & 0xffff0000u;
-  const float r2 = r1 - __uint_as_float(um);
-  hi = static_cast<uint16_t>(uh >> 16);
-  mid = static_cast<uint16_t>(um >> 16);
-  lo = static_cast<uint16_t>(__float_as_uint(r2) >> 16);
-}
-
-template <int TM>
-__global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __restrict__ h,
-                                                          const float* __restrict__ w,
-                                                          const float* __restrict__ bias,
-                                                          float* __restrict__ logits, int T, int d,
-                                                          int E) {
-  constexpr int NB = TM == 16 ? 1 : 4;      // 16 x 16 accumulators per wave
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][3][RT_TE * RT_TK];
+template <int TM, int EB, int KSPLIT, int PF>
+__global__ __launch_bounds__(64 * KSPLIT) void router_mfma_kernel(const uint16_t* __restrict__ h,
+                                                                 const float* __restrict__ w,
+                                                                 const float* __restrict__ bias,
+                                                                 float* __restrict__ logits, int T,
+                                                                 int d, int E) {
+  constexpr int TB = TM / 16;                      // token blocks per wave
+  constexpr int RT_TE = 16 * EB;                   // experts per workgroup
+  constexpr int NT = 64 * KSPLIT;
+  __shared__ float part[KSPLIT][TM * 16 * EB];     // per-wave partial tiles
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int t0 = blockIdx.x * TM, e0 = blockIdx.y * RT_TE;
+  const int kq = d / KSPLIT;                       // this wave's K range (multiple of 32)
+  const int kbeg = wv * kq;
 
-  // W staging: thread -> expert tid/4, k chunk (tid%4)*8
-  const int se = tid >> 2, sk = (tid & 3) * 8;
-  const bool se_ok = e0 + se < E;
-  const float* wsrc = w + static_cast<size_t>(se_ok ? e0 + se : 0) * d + sk;
-  float4 wa, wb;
-  auto load_w = [&](int k0) {
-    if (se_ok) {
-      wa = *reinterpret_cast<const float4*>(wsrc + k0);
-      wb = *reinterpret_cast<const float4*>(wsrc + k0 + 4);
-    } else {
-      wa = make_float4(0, 0, 0, 0);
-      wb = wa;
-    }
-  };
-  auto store_w = [&](int buf) {
-    const float v[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-    uint16_t t[3][8];
+  // fragment coordinates: row (lane % 16) of a 16-block.  The MFMA only needs A and
+  // B to use the same K order, so lane group g = lane / 16 holds the 8 K values
+  // {4g..4g+3, 16+4g..16+4g+3} of each 32-wide step: one 16-byte load per operand
+  // half then covers 64 contiguous bytes of a W_r row across the 4 groups.
+  const int frow = lane & 15, fk = (lane >> 4) * 4;
+  const uint16_t* ap[TB];
+  bool a_ok[TB];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) split3(v[j], t[0][j], t[1][j], t[2][j]);
+  for (int b = 0; b < TB; ++b) {
+    const int t = t0 + 16 * b + frow;
+    a_ok[b] = t < T;
+    ap[b] = h + static_cast<size_t>(a_ok[b] ? t : 0) * d + kbeg + fk;
+  }
+  const float* wp[EB];
+  bool w_ok[EB];
 #pragma unroll
-    for (int x = 0; x < 3; ++x) {
-      uint4 pk;
-      pk.x = t[x][0] | (uint32_t(t[x][1]) << 16);
-      pk.y = t[x][2] | (uint32_t(t[x][3]) << 16);
-      pk.z = t[x][4] | (uint32_t(t[x][5]) << 16);
-      pk.w = t[x][6] | (uint32_t(t[x][7]) << 16);
-      *reinterpret_cast<uint4*>(&Bs[buf][x][bs_index(se, sk >> 3)]) = pk;
-    }
-  };
+  for (int c = 0; c < EB; ++c) {
+    const int e = e0 + 16 * c + frow;
+    w_ok[c] = e < E;
+    wp[c] = w + static_cast<size_t>(w_ok[c] ? e : 0) * d + kbeg + fk;
+  }
 
-  // A fragments: lane holds token row (lane % 16) of its 16-token block, k (lane/16)*8..+8
-  const int tok_base = TM == 16 ? t0 : t0 + 16 * wv;
-  const int arow = lane & 15, ak = (lane >> 4) * 8;
-  const int tok = tok_base + arow;
-  const bool tok_ok = tok < T;
-  const uint16_t* asrc = h + static_cast<size_t>(tok_ok ? tok : 0) * d + ak;
-  uint4 afrag;
-  auto load_a = [&](int k0) {
-    afrag = tok_ok ? *reinterpret_cast<const uint4*>(asrc + k0) : make_uint4(0, 0, 0, 0);
-  };
+  f32x4_t acc[TB][EB];
+#pragma unroll
+  for (int b = 0; b < TB; ++b)
+#pragma unroll
+    for (int c = 0; c < EB; ++c) acc[b][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  f32x4_t acc[NB];
+  // PF K steps per round: every load of the round is issued before any is used
+  for (int k0 = 0; k0 < kq; k0 += PF * RT_TK) {
+    uint4 av[PF][TB];
+    float4 wlo[PF][EB], whi[PF][EB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = d / RT_TK;
-  load_w(0);
-  load_a(0);
-  store_w(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, afrag);
-    if (kt + 1 < nk) {
-      load_w((kt + 1) * RT_TK);
-      load_a((kt + 1) * RT_TK);
-    }
+    for (int q = 0; q < PF; ++q) {
+      const int k = k0 + q * RT_TK;
+      const bool in = k < kq;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int erow = (TM == 16 ? 16 * wv : 16 * b) + (lane & 15);
+      for (int b = 0; b < TB; ++b) {
+        uint2 lo = make_uint2(0, 0), hi = lo;
+        if (in && a_ok[b]) {
+          lo = *reinterpret_cast<const uint2*>(ap[b] + k);
+          hi = *reinterpret_cast<const uint2*>(ap[b] + k + 16);
+        }
+        av[q][b] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
 #pragma unroll
-      for (int x = 0; x < 3; ++x) {
-        const bf16x8_t bf = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][x][bs_index(erow, ak >> 3)]);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bf, acc[b], 0, 0, 0);
+      for (int c = 0; c < EB; ++c) {
+        const bool ok = in && w_ok[c];
+        wlo[q][c] = ok ? *reinterpret_cast<const float4*>(wp[c] + k) : make_float4(0, 0, 0, 0);
+        whi[q][c] = ok ? *reinterpret_cast<const float4*>(wp[c] + k + 16) : make_float4(0, 0, 0, 0);
       }
     }
-    if (kt + 1 < nk) store_w(buf ^ 1);
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PF; ++q) {
+#pragma unroll
+      for (int c = 0; c < EB; ++c) {
+        bf16x8_t w0, w1, w2;
+        split3x8(wlo[q][c], whi[q][c], w0, w1, w2);
+#pragma unroll
+        for (int b = 0; b < TB; ++b) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, av[q][b]);
+          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w0, acc[b][c], 0, 0, 0);
+          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w1, acc[b][c], 0, 0, 0);
+          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w2, acc[b][c], 0, 0, 0);
+        }
+      }
+    }
   }
   // accumulator: lane l, register r -> token row 4 (l/16) + r, expert column l % 16
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int e = e0 + (TM == 16 ? 16 * wv : 16 * b) + (lane & 15);
-    if (e >= E) continue;
-    const float be = bias ? bias[e] : 0.0f;
+  for (int b = 0; b < TB; ++b)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = tok_base + 4 * (lane >> 4) + r;
-      if (t < T) logits[static_cast<size_t>(t) * E + e] = acc[b][r] + be;
+    for (int c = 0; c < EB; ++c)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        part[wv][(16 * b + 4 * (lane >> 4) + r) * RT_TE + 16 * c + (lane & 15)] = acc[b][c][r];
+  __syncthreads();
+  for (int x = tid; x < TM * RT_TE; x += NT) {
+    const int t = t0 + x / RT_TE, e = e0 + x % RT_TE;
+    if (t < T && e < E) {
+      float s = part[0][x];
+#pragma unroll
+      for (int q = 1; q < KSPLIT; ++q) s += part[q][x];
+      logits[static_cast<size_t>(t) * E + e] = s + (bias ? bias[e] : 0.0f);
     }
   }
 }
@@ -138,13 +149,18 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(const uint16_t* __rest
 
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
                   int d, int E, hipStream_t s) {
-  const int ne = (E + RT_TE - 1) / RT_TE;
+  // A workgroup's loads all pass through one CU, so tiles are sized to spread the
+  // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves;
+  // large T uses 64 x 64 tiles so each W_r fragment feeds 4 token blocks.
   if (T >= 4096) {
-    hipLaunchKernelGGL(router_mfma_kernel<64>, dim3((T + 63) / 64, ne), dim3(256), 0, s, h, w, bias,
-                       logits, T, d, E);
+    hipLaunchKernelGGL((router_mfma_kernel<64, 4, 4, 2>), dim3((T + 63) / 64, (E + 63) / 64),
+                       dim3(256), 0, s, h, w, bias, logits, T, d, E);
+  } else if (d % (RT_TK * 16) == 0) {
+    hipLaunchKernelGGL((router_mfma_kernel<16, 1, 16, 4>), dim3((T + 15) / 16, (E + 15) / 16),
+                       dim3(1024), 0, s, h, w, bias, logits, T, d, E);
   } else {
-    hipLaunchKernelGGL(router_mfma_kernel<16>, dim3((T + 15) / 16, ne), dim3(256), 0, s, h, w, bias,
-                       logits, T, d, E);
+    hipLaunchKernelGGL((router_mfma_kernel<16, 1, 4, 4>), dim3((T + 15) / 16, (E + 15) / 16),
+                       dim3(256), 0, s, h, w, bias, logits, T, d, E);
   }
   return launch_status();
 }

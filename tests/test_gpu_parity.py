@@ -494,3 +494,29 @@ def test_one_expert_takes_every_token(torch):
     wg, wu, wd = w.w_gate(), w.w_up(), w.w_down()
     ref = oracle.moe_layer(w.h, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
     layer_tolerance_check(out, ref, "one expert")
+
+
+@pytest.mark.parametrize("case", ["lladamoe_t1024_e64", "llada2mini_t4096_e256", "fuzz_d128_f64",
+                                  "fuzz_d384_f192"])
+def test_packed_weights_give_bitwise_identical_layer(torch, case):
+    # the packed layout only changes where the GEMM reads each weight slice from;
+    # every product and sum is the same, so the outputs must match bit for bit
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    if case.startswith("fuzz"):
+        d, f = (int(x[1:]) for x in case.split("_")[1:])
+        w = make_fuzz_workload(300 + d, T=900, d=d, E=12, f=f, k_max=6)
+        dv = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()),
+              "w_down": to_device(w.w_down()), "w_router": to_device(w.w_router()),
+              "router_bias": None if w.router_bias is None else to_device(w.router_bias)}
+    else:
+        w = workload(case)
+        dv = dict(dev_weights(case))
+    outs = []
+    for packed in (False, True):
+        ew = ExpertWeights(**dv)
+        if packed:
+            ew.pack()
+        lay = MoELayer(w.T, w.d, ew, w.params)
+        outs.append(bf16_bits(lay.forward(to_device(w.h), TokenState(**state_tensors(w)))))
+        torch.cuda.synchronize()
+    assert np.array_equal(outs[0], outs[1])
