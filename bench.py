@@ -17,9 +17,12 @@ baseline.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import csv
 import ctypes
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,6 +33,10 @@ METRIC = "MoE-layer tokens/s + TFLOP/s (alloc. expert FLOPs) as % bf16 MFMA peak
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 DEFAULT_WORKLOAD = "lladamoe_t1024_e64"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+COPY_CAL_BYTES = 1 << 28       # the plain device copy that calibrates the byte counters
+# rocprofv3 kernel names of the stages with a counter-derived traffic figure
+STAGE_KERNELS = {"gemm_up": "swiglu_gemm_kernel<true>", "gemm_down": "swiglu_gemm_kernel<false>"}
 
 
 def log(msg):
@@ -125,6 +132,101 @@ def stage_roofline(stage, ms, d, f, P, touched, T, E):
     return {"kernel": stage, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
             "algorithmic_bytes": int(nbytes), "algorithmic_flops": int(flops), "ms": round(ms, 5)}
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the sources of the grouped GEMM (its kernel and shared header): a
+    stored counter reading is valid only for the kernel it was taken on."""
+    hsh = hashlib.sha256()
+    for rel in ("gemm.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2608_01784_amd", "csrc", rel), "rb") as fh:
+            hsh.update(fh.read())
+    return hsh.hexdigest()
+
+
+def _counter_rows(path):
+    """(kernel name, counter, value) of every dispatch in a rocprofv3 counter CSV."""
+    rows = []
+    with open(path, newline="") as fh:
+        for r in csv.DictReader(fh):
+            name = r["Kernel_Name"].replace("void ", "").replace("rfx::(anonymous namespace)::", "")
+            name = re.sub(r"\(.*", "", name)
+            rows.append((name, r["Counter_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def _per_dispatch_kib(path, counter, kernel=None):
+    """Mean counter value (KiB) per dispatch of `kernel`; without a kernel name, of the
+    dispatches with the largest reading (the calibration copy)."""
+    vals = [(n, v) for n, c, v in _counter_rows(path) if c == counter]
+    if kernel is None:
+        top = max(v for _, v in vals)
+        sel = [v for _, v in vals if v >= 0.5 * top]
+    else:
+        sel = [v for n, v in vals if n == kernel]
+    if not sel:
+        raise SystemExit(f"no {counter} dispatches of {kernel or 'the copy'} in {path}")
+    return sum(sel) / len(sel), len(sel)
+
+
+def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+    """Turn two rocprofv3 --pmc runs of the bench (FETCH_SIZE, WRITE_SIZE) and the same two
+    counters on a plain copy of COPY_CAL_BYTES into HBM bytes per GEMM launch, stored in
+    the traffic file under the current GEMM source digest."""
+    cf, _ = _per_dispatch_kib(copy_fetch_csv, "FETCH_SIZE")
+    cw, _ = _per_dispatch_kib(copy_write_csv, "WRITE_SIZE")
+    k_fetch = COPY_CAL_BYTES / (cf * 1024.0)      # true read bytes per counted byte
+    k_write = COPY_CAL_BYTES / (cw * 1024.0)
+    data = {"calibration": {}, "entries": []}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            data = json.load(fh)
+    data["calibration"] = {"copy_bytes": COPY_CAL_BYTES, "fetch_kib": round(cf, 1),
+                           "write_kib": round(cw, 1), "fetch_factor": round(k_fetch, 4),
+                           "write_factor": round(k_write, 4)}
+    digest = kernel_source_digest()
+    for stage, kname in STAGE_KERNELS.items():
+        fk, nf = _per_dispatch_kib(fetch_csv, "FETCH_SIZE", kname)
+        wk, nw = _per_dispatch_kib(write_csv, "WRITE_SIZE", kname)
+        ent = {"workload": workload, "expert_weights": layout, "kernel": stage,
+               "kernel_name": kname, "source_sha256": digest,
+               "fetch_kib_per_dispatch": round(fk, 1), "write_kib_per_dispatch": round(wk, 1),
+               "dispatches": [nf, nw],
+               "read_bytes": int(fk * 1024 * k_fetch), "write_bytes": int(wk * 1024 * k_write)}
+        ent["traffic_bytes"] = ent["read_bytes"] + ent["write_bytes"]
+        data["entries"] = [e for e in data["entries"]
+                           if (e["workload"], e["expert_weights"], e["kernel"]) != (workload, layout, stage)]
+        data["entries"].append(ent)
+        print(json.dumps(ent))
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(data, fh, indent=1)
+        fh.write("\n")
+
+
+def measured_traffic(workload, layout, stage):
+    """HBM bytes per launch from stored counter readings, or None when there are none for
+    this workload and kernel or the kernel source has changed since they were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as fh:
+        data = json.load(fh)
+    digest = kernel_source_digest()
+    for e in data.get("entries", []):
+        if (e["workload"], e["expert_weights"], e["kernel"]) == (workload, layout, stage):
+            return e["traffic_bytes"] if e["source_sha256"] == digest else None
+    return None
+
+
+def copy_calibration():
+    """The plain device copy of COPY_CAL_BYTES whose counter readings scale FETCH_SIZE and
+    WRITE_SIZE to bytes (run under rocprofv3 --pmc)."""
+    import torch
+    src = torch.ones(COPY_CAL_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_CAL_BYTES, "copies": 3}))
 
 
 def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: HipEvents):
@@ -226,7 +328,16 @@ def main():
     ap.add_argument("--no-uniform", action="store_true")
     ap.add_argument("--packed-weights", action="store_true",
                     help="pack the expert weights once (reflex_pack_*) and stream the packed layout")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only the plain 256 MiB device copy that calibrates the byte counters")
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                      "COPY_WRITE_CSV"),
+                    help="store HBM traffic per GEMM launch from rocprofv3 counter CSVs (no GPU)")
     a = ap.parse_args()
+    layout = "packed at load" if a.packed_weights else "row-major"
+    if a.ingest_pmc:
+        ingest_pmc(a.workload, layout, *a.ingest_pmc)
+        return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(no collectives, no sharding); run with --gpus 1.", file=sys.stderr)
@@ -242,6 +353,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if a.copy_calibration:
+        copy_calibration()
+        return
     _lib.lib()
     log(f"generating {a.workload} (seed {a.seed})")
     w = make_workload(a.workload, seed=a.seed)
@@ -289,6 +403,11 @@ def main():
     stages = var["stage_ms"]
     dom = max(("gemm_up", "gemm_down", "router", "combine", "topk", "permute"), key=lambda s: stages[s])
     roof = stage_roofline(dom, stages[dom], d, f, P, touched, T, E)
+    roof_all = {s: stage_roofline(s, stages[s], d, f, P, touched, T, E)
+                for s in ("gemm_up", "gemm_down", "router", "topk", "permute", "combine")}
+    for s in STAGE_KERNELS:
+        roof_all[s]["traffic"] = measured_traffic(w.name, layout, s)
+    roof["traffic"] = roof_all[dom]["traffic"]
     out = {
         "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(step_ms, 4),
@@ -297,15 +416,14 @@ def main():
         "config": {"workload": w.name, "tokens": T, "hidden": d, "experts": E, "expert_ffn": f,
                    "shared_ffn": w.f_shared, "layers": L, "k_base": w.params.k_base,
                    "k_range": [w.params.k_min, w.params.k_max], "path": "variable-K (REFLEX)",
-                   "expert_weights": "packed at load" if a.packed_weights else "row-major"},
+                   "expert_weights": layout},
         "alloc_tflops": round(alloc_tflops, 2),
         "pct_bf16_peak": round(100 * alloc_tflops / PEAK_BF16_TFLOPS, 2),
         "pairs_per_layer": P, "avg_k": round(P / T, 4), "experts_touched": touched,
         "max_expert_rows": int(counts.max()), "gpu_ms_per_step": round(var["gpu_ms"], 4),
         "stage_ms": {k: round(v, 5) for k, v in stages.items()},
         "roofline": roof,
-        "roofline_all": {s: stage_roofline(s, stages[s], d, f, P, touched, T, E)
-                         for s in ("gemm_up", "gemm_down", "router", "topk", "permute", "combine")},
+        "roofline_all": roof_all,
     }
     if uni is not None:
         lu = uni["layers"][0]

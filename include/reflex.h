@@ -243,7 +243,9 @@ int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
  *                  shares k_i across MoE layers, Section 3.3);
  *   uniform_k > 0  default fixed token-choice routing, k_i = uniform_k;
  *   otherwise      reflex_assign_budget with `params` and the token state.
- * Pair capacity is T * kcap with kcap = uniform_k if uniform_k > 0, else params.k_max.
+ * Pair capacity is T * kcap with kcap = uniform_k if uniform_k > 0, else params.k_max;
+ * counts (k_in included) are clamped to [0, kcap].  `params` is validated only when
+ * uniform_k <= 0.
  */
 typedef struct {
   int32_t T, d, E, f;

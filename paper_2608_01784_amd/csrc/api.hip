@@ -261,9 +261,11 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
                         static_cast<const void*>(a->logits_out)})
     RFX_TRY(check_opt_ptr(p, 4));
   if (fs) RFX_TRY(check_ptrs({a->ws_gate, a->ws_up, a->ws_down}, 16));
+  // pair capacity T * kcap: kcap = uniform_k when set (caller counts are then clamped
+  // to it), else params.k_max
   int kcap;
   const bool budget = a->k_in == nullptr && a->uniform_k <= 0;
-  if (a->k_in == nullptr && a->uniform_k > 0) {
+  if (a->uniform_k > 0) {
     kcap = a->uniform_k;
   } else {
     RFX_TRY(check_params(&a->params));

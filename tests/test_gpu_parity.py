@@ -446,6 +446,18 @@ def test_reused_counts_and_zero_count_tokens(torch):
     compare_layer(name, out, k, logits, tag=" k_in")
 
 
+def test_reused_counts_clamped_to_uniform_capacity(torch):
+    # uniform_k > 0 sets the pair capacity (T * uniform_k) even when counts are passed in;
+    # the caller's counts are then clamped to uniform_k
+    name = "tiny_t128_e8"
+    w = workload(name)
+    k = np.random.default_rng(6).integers(0, w.params.k_max + 1, w.T)
+    out, _, pairs, logits = fused(torch, name, uniform_k=2, k_in=k)
+    kc = np.minimum(k, 2)
+    assert pairs == int(kc.sum())
+    compare_layer(name, out, kc, logits, tag=" k_in clamped")
+
+
 def test_deterministic(torch):
     name = "llada2mini_t4096_e256"
     a = fused(torch, name)
