@@ -375,6 +375,8 @@ def main():
             ew.w_gate = ew.w_up = ew.w_down = None
         dws.append(ew)
         hosts.append(host if l == 0 else None)
+        if l > 0:
+            w.release(l)
         if w.n_layers > 1:
             log(f"layer {l} weights resident")
     residuals = [to_device(w.residual(l)) for l in range(w.n_layers)] if w.n_layers > 1 else None

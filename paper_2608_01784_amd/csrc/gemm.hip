@@ -59,6 +59,10 @@ constexpr int GM_B_ELEMS = GM_BROWS * GM_BK;   // B slice
 constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
 constexpr int GM_STAGES = RFX_GEMM_STAGES;
 constexpr int GM_XCDS = 8;
+#ifndef RFX_GEMM_OCC
+#define RFX_GEMM_OCC 1
+#endif
+constexpr int GM_OCC = RFX_GEMM_OCC;       // resident workgroups per CU (LDS ring permitting)
 constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per wave
 // LDS rows are BK bf16 = CH chunks of 16 bytes; one DMA op (a wave, 64 lanes x 16
 // bytes = 1 KB) fills ROWS_PER_OP whole rows.  Chunk c of row r sits in slot
@@ -141,7 +145,8 @@ __device__ __forceinline__ void lds_barrier() {
 
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
-__global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
+__global__ __launch_bounds__(GM_THREADS) __attribute__((amdgpu_waves_per_eu(GM_OCC, GM_OCC)))
+void swiglu_gemm_kernel(
     const uint16_t* __restrict__ x,            // UP: h [T, K]; DOWN: act [rows, K]
     const int32_t* __restrict__ gather,        // UP: sorted_token or NULL (identity)
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ expert_offsets, int E,
@@ -279,36 +284,54 @@ __global__ __launch_bounds__(GM_THREADS, 1) void swiglu_gemm_kernel(
 #pragma unroll
         for (int j = 0; j < GM_NT; ++j)
           bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
+        // weights as the MFMA's A operand: the accumulator is the transposed tile,
+        // so each lane ends up holding 4 consecutive output columns of one row
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < GM_NT; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
       }
     }
-    // epilogue: lane l, register r holds row 8 (r/4) + 4 (l/32) + r%4, column l%32
+    // epilogue: lane l, register r holds output row l % 32 (a pair row) and column
+    // 8 (r/4) + 4 (l/32) + r%4 of its 32 x 32 block, so registers 4g..4g+3 are 4
+    // consecutive columns: one 8-byte store each.  N is a multiple of 64, so a
+    // group of 4 is either wholly inside a partial last N tile or wholly past it.
     const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E,
                                    dense_M, n_tiles, out_rows);
-    const int col = lane & 31;
+    const int ccol = 4 * (lane >> 5);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
+      const int grow = t.row0 + a_row[i] + (lane & 31);
+      if (grow >= t.row_end) continue;
+      uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
+      if (UP) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int grow = t.row0 + a_row[i] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (grow >= t.row_end) continue;
-        uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
-        if (UP) {
+        for (int j = 0; j < GM_NT / 2; ++j) {
 #pragma unroll
-          for (int j = 0; j < GM_NT / 2; ++j) {
-            const int c = wn * (GM_BROWS / 4) + 32 * j + col;
-            const float g = acc[i][j][r], u = acc[i][j + GM_NT / 2][r];
-            if (t.n0 + c < N_out) orow[c] = f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          for (int g = 0; g < 4; ++g) {
+            const int c = wn * (GM_BROWS / 4) + 32 * j + 8 * g + ccol;
+            float a4[4];
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const float gg = acc[i][j][4 * g + h], uu = acc[i][j + GM_NT / 2][4 * g + h];
+              a4[h] = gg / (1.0f + expf(-gg)) * uu;
+            }
+            if (t.n0 + c < N_out)
+              *reinterpret_cast<uint2*>(orow + c) =
+                  make_uint2(pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3]));
           }
-        } else {
+        }
+      } else {
 #pragma unroll
-          for (int j = 0; j < GM_NT; ++j) {
-            const int c = wn * (GM_BROWS / 2) + 32 * j + col;
-            if (t.n0 + c < N_out) orow[c] = f32_to_bf16(acc[i][j][r]);
+        for (int j = 0; j < GM_NT; ++j) {
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int c = wn * (GM_BROWS / 2) + 32 * j + 8 * g + ccol;
+            const f32x16_t& a = acc[i][j];
+            if (t.n0 + c < N_out)
+              *reinterpret_cast<uint2*>(orow + c) =
+                  make_uint2(pack_bf16x2(a[4 * g], a[4 * g + 1]), pack_bf16x2(a[4 * g + 2], a[4 * g + 3]));
           }
         }
       }
@@ -392,7 +415,7 @@ int persistent_grid() {
     else
       cus = 256;
   }
-  return (cus + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
+  return (cus * GM_OCC + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
 }
 
 template <bool UP>

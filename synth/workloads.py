@@ -157,6 +157,11 @@ class Workload:
             list(ex.map(job, range(E)))
         return out
 
+    def release(self, layer: int) -> None:
+        """Drop the cached stacked weights of one layer (after they were uploaded)."""
+        for which in (_TAG_WG, _TAG_WU, _TAG_WD):
+            self._cache.pop(("stack", layer, which), None)
+
     def w_gate(self, layer: int = 0) -> np.ndarray:
         """[E, f, d] bf16 bits (nn.Linear layout, d contiguous)."""
         return self._stacked(layer, _TAG_WG)
