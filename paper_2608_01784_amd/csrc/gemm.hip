@@ -9,31 +9,35 @@
 // (tile_off) cuts each expert's rows into 128-row M tiles, so no launch shape
 // depends on the device-resident per-expert counts.
 //
-// Tile 128 (M) x GM_BROWS (weight rows, 256) x 64 (K); 4 waves in 2 x 2, each
-// 64 x GM_BROWS/2 as 2 x GM_NT v_mfma_f32_32x32x16_bf16 tiles with fp32
-// accumulators.  In the up GEMM the first half of the weight rows are gate rows and
-// the second half the matching up rows, so gate and up of one output column meet
-// in the same lane and register and SiLU(g) * u is formed before the single bf16
-// rounding of the activation.  A partial last N tile clamps its weight rows and
-// skips the stores past N.
+// Tile 128 (M) x GM_BROWS (256 weight rows) x 64 (K) on v_mfma_f32_32x32x16_bf16
+// with fp32 accumulators: 4 compute waves in 2 x 2, each 64 x 128, plus 4 waves
+// that only issue the global->LDS copies (one of each kind per SIMD), so a wave
+// waiting for room in the memory queue never holds up the matrix cores.
+// In the up GEMM the first half of the weight rows are gate rows and the second
+// half the matching up rows, so gate and up of one output column meet in the same
+// lane and register and SiLU(g) * u is formed before the single bf16 rounding of
+// the activation.  A partial last N tile clamps its weight rows and skips the
+// stores past N.
 //
 // Data movement: operands go from global memory straight into LDS with
-// global_load_lds_dwordx4 (16 bytes per lane, no register staging) through a
-// ring of GM_STAGES K-slices, so GM_STAGES-1 slices are in flight while one is
-// multiplied.  Rows are 128 bytes (8 chunks of 16 bytes) with chunk c of row r
-// stored in slot c ^ ((r / 2) % 8).  The LDS has 64 four-byte banks and serves a
-// 16-byte read for 16 lanes at a time, i.e. 16 rows of one fragment: their
-// (row parity, slot) pairs are all distinct, so fragment reads are conflict-free,
-// while a wave's DMA still writes 1 KB (8 whole rows) contiguously.
+// global_load_lds_dwordx4 (16 bytes per lane, no register staging) through a ring
+// of GM_STAGES K-slices, so GM_STAGES-1 slices are in flight while one is multiplied.
+// Rows are 128 bytes (8 chunks of 16 bytes) with chunk c of row r stored in slot
+// c ^ ((r / 2) % 8).  The LDS has 64 four-byte banks and serves a 16-byte read
+// for 16 lanes at a time, i.e. 16 rows of one fragment: their (row parity, slot)
+// pairs are all distinct, so fragment reads are conflict-free, while a wave's DMA
+// still writes 1 KB (8 whole rows) contiguously.
 //
 // Scheduling: a persistent grid (one workgroup per CU) walks a flattened
 // sequence of (tile, K-slice) steps, so prefetching continues across tile
 // boundaries.  Tiles are dealt to the 8 XCDs in contiguous runs (workgroup b
-// runs on XCD b % 8), so one expert's tiles share that XCD's L2: the gathered
-// input rows and each weight tile are fetched from memory once.
+// runs on XCD b % 8), so one expert's tiles share that XCD's L2.  Within an
+// expert the N tiles of one M tile are adjacent, so the workgroups of an XCD
+// working at the same time share each gathered input slice and each weight slice.
 #include "common.h"
 
 namespace rfx {
+
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -45,25 +49,19 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 #ifndef RFX_GEMM_STAGES
 #define RFX_GEMM_STAGES 3
 #endif
-constexpr int GM_BM = kGemmBM;
 #ifndef RFX_GEMM_BK
 #define RFX_GEMM_BK 64
 #endif
+#ifndef RFX_GEMM_NINNER
+#define RFX_GEMM_NINNER 1
+#endif
 constexpr int GM_BK = RFX_GEMM_BK;         // K per pipeline step: 64 or 32
-constexpr int GM_THREADS = 256;
 constexpr int GM_BROWS = RFX_GEMM_BROWS;   // weight (B) rows per tile: 128 or 256
 constexpr int GM_UP_BN = GM_BROWS / 2;     // activation columns per up-GEMM tile (gate + up rows)
 constexpr int GM_DOWN_BN = GM_BROWS;       // output columns per down-GEMM tile
-constexpr int GM_A_ELEMS = GM_BM * GM_BK;      // A slice: 128 rows x BK
 constexpr int GM_B_ELEMS = GM_BROWS * GM_BK;   // B slice
-constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
-constexpr int GM_STAGES = RFX_GEMM_STAGES;
 constexpr int GM_XCDS = 8;
-#ifndef RFX_GEMM_OCC
-#define RFX_GEMM_OCC 1
-#endif
-constexpr int GM_OCC = RFX_GEMM_OCC;       // resident workgroups per CU (LDS ring permitting)
-constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per wave
+constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per compute wave
 // LDS rows are BK bf16 = CH chunks of 16 bytes; one DMA op (a wave, 64 lanes x 16
 // bytes = 1 KB) fills ROWS_PER_OP whole rows.  Chunk c of row r sits in slot
 // c ^ ((r / RG) % CH), RG = 16 / CH: the 16 rows one 16-lane group reads cover all
@@ -71,22 +69,31 @@ constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per wave
 constexpr int GM_CH = GM_BK / 8;
 constexpr int GM_ROWS_PER_OP = 64 / GM_CH;
 constexpr int GM_RG = 16 / GM_CH;
-constexpr int GM_A_OPS = GM_BM / GM_ROWS_PER_OP / 4;      // DMA ops per wave per step for A
+constexpr int GM_BM = kGemmBM;
+constexpr int GM_THREADS = 512;            // 4 compute + 4 loading waves
+constexpr int GM_STAGES = RFX_GEMM_STAGES;
+constexpr int GM_A_ELEMS = GM_BM * GM_BK;
+constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
+constexpr int GM_A_OPS = GM_BM / GM_ROWS_PER_OP / 4;      // DMA ops per loading wave per step for A
 constexpr int GM_B_OPS = GM_BROWS / GM_ROWS_PER_OP / 4;   // ... and for B
-constexpr int GM_OPS = GM_A_OPS + GM_B_OPS;               // vector-memory ops per thread per step
+constexpr int GM_OPS = GM_A_OPS + GM_B_OPS;
+constexpr size_t GM_LDS = size_t(GM_STAGES) * GM_STAGE_ELEMS * sizeof(uint16_t);
 static_assert(GM_BK == 32 || GM_BK == 64, "BK");
 
 struct Tile {
   int expert, row0, row_end, n0;
 };
 
-// Logical tile L -> tile.  Routed: experts in order, within an expert the N tile
-// outer and the M tile inner (consecutive tiles share one weight slice).  Dense:
-// one expert over rows 0..dense_M-1.
+// Logical tile L -> tile.  Routed: experts in order, within an expert the M tile
+// outer and the N tile inner (or the reverse when RFX_GEMM_NINNER is 0).  Dense:
+// one expert over rows 0..dense_M-1.  tile_off and expert_offsets are the kernel's
+// LDS copies; the expert is found in one round: every lane tests up to 4 experts
+// and the wave counts those whose first tile lies at or before L (tile_off is
+// nondecreasing, so that count minus one is the expert).  L is wave-uniform.
 template <int BN>
-__device__ __forceinline__ Tile decode_tile(int L, const int32_t* __restrict__ tile_off,
-                                            const int32_t* __restrict__ expert_offsets, int E,
-                                            int dense_M, int n_tiles, int out_rows) {
+__device__ __forceinline__ Tile decode_tile(int L, const int32_t* tile_off,
+                                            const int32_t* expert_offsets, int E, int dense_M,
+                                            int n_tiles, int out_rows) {
   Tile t;
   if (dense_M >= 0) {
     const int mt = (dense_M + GM_BM - 1) / GM_BM;
@@ -96,16 +103,25 @@ __device__ __forceinline__ Tile decode_tile(int L, const int32_t* __restrict__ t
     t.row_end = dense_M;
     return t;
   }
-  int lo = 0, hi = E - 1;               // largest e with tile_off[e] * n_tiles <= L
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tile_off[mid] * n_tiles <= L) lo = mid; else hi = mid - 1;
+  const int lane = threadIdx.x & 63;
+  int cnt = 0;
+#pragma unroll
+  for (int q = 0; q < REFLEX_MAX_EXPERTS / 64; ++q) {
+    const int e = lane + 64 * q;
+    cnt += (e < E && tile_off[e] * n_tiles <= L) ? 1 : 0;
   }
+  int lo = wave_sum_i32(cnt) - 1;
+  lo = lo < 0 ? 0 : lo;
   const int local = L - tile_off[lo] * n_tiles;
-  const int mt = tile_off[lo + 1] - tile_off[lo];
   t.expert = lo;
+#if RFX_GEMM_NINNER
+  t.n0 = (local % n_tiles) * BN;
+  t.row0 = expert_offsets[lo] + (local / n_tiles) * GM_BM;
+#else
+  const int mt = tile_off[lo + 1] - tile_off[lo];
   t.n0 = (local / mt) * BN;
   t.row0 = expert_offsets[lo] + (local % mt) * GM_BM;
+#endif
   const int re = expert_offsets[lo + 1];
   t.row_end = re < out_rows ? re : out_rows;
   if (t.row0 < 0 || t.row0 >= t.row_end) t.row_end = t.row0;   // inconsistent offsets: no rows
@@ -120,8 +136,8 @@ __device__ __forceinline__ void waitcnt_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
 }
 
-// Each step issues GM_OPS vector-memory ops per thread; let the ops of `pending`
-// later steps stay outstanding.
+// Each step issues GM_OPS vector-memory ops per loading wave; let the ops of
+// `pending` later steps stay outstanding.
 __device__ __forceinline__ void wait_vm(int pending) {
   static_assert(GM_STAGES >= 2 && GM_STAGES <= 6, "stage count");
   switch (pending) {
@@ -131,6 +147,13 @@ __device__ __forceinline__ void wait_vm(int pending) {
     case 3: waitcnt_vm<(GM_STAGES > 4 ? 3 * GM_OPS : 0)>(); break;
     default: waitcnt_vm<(GM_STAGES > 5 ? 4 * GM_OPS : 0)>(); break;
   }
+}
+
+// One wave's 1 KB copy: 16 bytes per lane from `src` straight into LDS at `dst`
+// (the wave-uniform base; lane L lands at dst + 16 L bytes).  Kept out of line of
+// the kernel's lambdas so that the host-side pass of the kernel stays valid.
+__device__ __forceinline__ void lds_dma(const uint16_t* src, uint16_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
 }
 
 // Workgroup barrier without the release/acquire fences of __syncthreads(): those
@@ -145,8 +168,7 @@ __device__ __forceinline__ void lds_barrier() {
 
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
-__global__ __launch_bounds__(GM_THREADS) __attribute__((amdgpu_waves_per_eu(GM_OCC, GM_OCC)))
-void swiglu_gemm_kernel(
+__global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     const uint16_t* __restrict__ x,            // UP: h [T, K]; DOWN: act [rows, K]
     const int32_t* __restrict__ gather,        // UP: sorted_token or NULL (identity)
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ expert_offsets, int E,
@@ -159,7 +181,16 @@ void swiglu_gemm_kernel(
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = (N_out + BN - 1) / BN;     // the last N tile may be partial
-  const int total = dense_M >= 0 ? ((dense_M + GM_BM - 1) / GM_BM) * n_tiles : tile_off[E] * n_tiles;
+  // the tile plan and expert row offsets, copied to LDS once for the tile decodes
+  __shared__ int s_tile_off[REFLEX_MAX_EXPERTS + 1], s_eo[REFLEX_MAX_EXPERTS + 1];
+  if (dense_M < 0) {
+    for (int e = threadIdx.x; e <= E; e += blockDim.x) {
+      s_tile_off[e] = tile_off[e];
+      s_eo[e] = expert_offsets[e];
+    }
+    __syncthreads();
+  }
+  const int total = dense_M >= 0 ? ((dense_M + GM_BM - 1) / GM_BM) * n_tiles : s_tile_off[E] * n_tiles;
 
   // this workgroup's tiles: a contiguous run per XCD, strided over the XCD's workgroups
   const int xcd = blockIdx.x % GM_XCDS;
@@ -174,77 +205,86 @@ void swiglu_gemm_kernel(
   const int n_steps = n_my * nk;
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool producer = wave >= 4;
+  const int wv = wave & 3;          // index among the loading (and among the computing) waves
   const int wm = wv >> 1, wn = wv & 1;
 
-  // ---- loader (runs GM_STAGES-1 steps ahead of the multiply) ----
-  // op q of a wave fills rows R0 = 8 q' .. 8 q' + 7 (q' the op's global 8-row index);
-  // lane L writes row r = R0 + L / 8, slot L % 8, which must hold logical chunk
-  // c = (L % 8) ^ ((r / 2) % 8) = (L % 8) ^ (4 (q' % 2) + L / 16).
-  auto lane_row = [&](int q) { return q * GM_ROWS_PER_OP + lane / GM_CH; };
-  auto lane_chunk = [&](int q) {
-    return ((lane % GM_CH) ^ ((lane_row(q) / GM_RG) % GM_CH)) * 8;
-  };
-  const uint16_t* a_ptr[GM_A_OPS];
-  const uint16_t* b_ptr[GM_B_OPS];
-  int ld_tile = -1;
-  auto setup_loader = [&](int tile_i) {
-    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E, dense_M,
-                                   n_tiles, out_rows);
-    const int rows_valid = t.row_end - t.row0;
+  if (producer) {
+    // ---- loading waves: run GM_STAGES-1 steps ahead of the multiply ----
+    // op q of a wave fills rows R0 = ROWS_PER_OP q' .. (q' the op's global row-group
+    // index); lane L writes row r = R0 + L / CH, slot L % CH, which must hold
+    // logical chunk c = (L % CH) ^ ((r / RG) % CH).
+    auto lane_row = [&](int q) { return q * GM_ROWS_PER_OP + lane / GM_CH; };
+    auto lane_chunk = [&](int q) {
+      return ((lane % GM_CH) ^ ((lane_row(q) / GM_RG) % GM_CH)) * 8;
+    };
+    const uint16_t* a_ptr[GM_A_OPS];
+    const uint16_t* b_ptr[GM_B_OPS];
+    int ld_tile = -1;
+    auto setup_loader = [&](int tile_i) {
+      const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
+                                     n_tiles, out_rows);
+      const int rows_valid = t.row_end - t.row0;
 #pragma unroll
-    for (int j = 0; j < GM_A_OPS; ++j) {
-      const int r = lane_row(GM_A_OPS * wv + j);
-      int src = t.row0 + (r < rows_valid ? r : 0);     // rows past the expert reuse row0
-      if (rows_valid <= 0) src = 0;
-      if (UP && gather != nullptr) {
-        src = gather[src];
-        src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
+      for (int j = 0; j < GM_A_OPS; ++j) {
+        const int r = lane_row(GM_A_OPS * wv + j);
+        int src = t.row0 + (r < rows_valid ? r : 0);     // rows past the expert reuse row0
+        if (rows_valid <= 0) src = 0;
+        if (UP && gather != nullptr) {
+          src = gather[src];
+          src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
+        }
+        a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(GM_A_OPS * wv + j);
       }
-      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(GM_A_OPS * wv + j);
-    }
-    if (packed) {
-      const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
+      if (packed) {
+        const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
 #pragma unroll
-      for (int j = 0; j < GM_B_OPS; ++j)
-        b_ptr[j] = w0 + slice0 * GM_B_ELEMS + (GM_B_OPS * wv + j) * 512 + lane * 8;
-      return;
-    }
-#pragma unroll
-    for (int j = 0; j < GM_B_OPS; ++j) {
-      const int r = lane_row(GM_B_OPS * wv + j);
-      const uint16_t* wb;
-      int wr;
-      if (UP) {     // rows [0, BROWS/2): gate rows n0 + r; the rest: up rows n0 + r - BROWS/2
-        wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
-        wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
-      } else {
-        wb = w0 + t.expert * w_expert_stride;
-        wr = t.n0 + r;
+        for (int j = 0; j < GM_B_OPS; ++j)
+          b_ptr[j] = w0 + slice0 * GM_B_ELEMS + (GM_B_OPS * wv + j) * 512 + lane * 8;
+        return;
       }
-      wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
-      b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(GM_B_OPS * wv + j);
-    }
-  };
-  auto issue = [&](int step) {
-    const int tile_i = step / nk, kt = step - tile_i * nk;
-    if (tile_i != ld_tile) {
-      setup_loader(tile_i);
-      ld_tile = tile_i;
-    }
-    uint16_t* As = smem + (step % GM_STAGES) * GM_STAGE_ELEMS;
-    uint16_t* Bs = As + GM_A_ELEMS;
-    const int k0 = kt * GM_BK;
-    const size_t kb = packed ? static_cast<size_t>(kt) * GM_B_ELEMS : static_cast<size_t>(k0);
 #pragma unroll
-    for (int j = 0; j < GM_A_OPS; ++j)
-      __builtin_amdgcn_global_load_lds(a_ptr[j] + k0, As + (GM_A_OPS * wv + j) * 512, 16, 0, 0);
+      for (int j = 0; j < GM_B_OPS; ++j) {
+        const int r = lane_row(GM_B_OPS * wv + j);
+        const uint16_t* wb;
+        int wr;
+        if (UP) {     // rows [0, BROWS/2): gate rows n0 + r; the rest: up rows n0 + r - BROWS/2
+          wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
+          wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
+        } else {
+          wb = w0 + t.expert * w_expert_stride;
+          wr = t.n0 + r;
+        }
+        wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
+        b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(GM_B_OPS * wv + j);
+      }
+    };
+    auto issue = [&](int step) {
+      const int tile_i = step / nk, kt = step - tile_i * nk;
+      if (tile_i != ld_tile) {
+        setup_loader(tile_i);
+        ld_tile = tile_i;
+      }
+      uint16_t* As = smem + (step % GM_STAGES) * GM_STAGE_ELEMS;
+      uint16_t* Bs = As + GM_A_ELEMS;
+      const int k0 = kt * GM_BK;
+      const size_t kb = packed ? static_cast<size_t>(kt) * GM_B_ELEMS : static_cast<size_t>(k0);
 #pragma unroll
-    for (int j = 0; j < GM_B_OPS; ++j)
-      __builtin_amdgcn_global_load_lds(b_ptr[j] + kb, Bs + (GM_B_OPS * wv + j) * 512, 16, 0, 0);
-  };
+      for (int j = 0; j < GM_A_OPS; ++j) lds_dma(a_ptr[j] + k0, As + (GM_A_OPS * wv + j) * 512);
+#pragma unroll
+      for (int j = 0; j < GM_B_OPS; ++j) lds_dma(b_ptr[j] + kb, Bs + (GM_B_OPS * wv + j) * 512);
+    };
+    for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
+    for (int s = 0; s < n_steps; ++s) {
+      wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
+      lds_barrier();       // slice s visible to all waves; slice s-1 no longer read
+      if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
+    }
+    return;
+  }
 
-  // ---- multiply ----
+  // ---- compute waves ----
   // B sub-tiles of this wave (32 rows each).  UP: the first GM_NT/2 are gate rows
   // wn*BROWS/4 + 32j, the rest the matching up rows (+ BROWS/2), so sub-tile j and
   // j + GM_NT/2 hold gate and up of the same output columns.  DOWN: wn*BROWS/2 + 32j.
@@ -255,12 +295,10 @@ void swiglu_gemm_kernel(
                                    : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - GM_NT / 2))
                   : wn * (GM_BROWS / 2) + 32 * j;
   const int a_row[2] = {wm * 64, wm * 64 + 32};
-  // fragment rows are 32-aligned bases + (lane % 32): (row / 2) % 8 = (lane / 2) % 8
+  // fragment rows are 32-aligned bases + (lane % 32): (row / RG) % CH from lane % 32
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / GM_RG) % GM_CH;
   f32x16_t acc[2][GM_NT];
-
-  for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
-  int s = 0;        // flattened step; loads run GM_STAGES-1 steps ahead, across tiles
+  int s = 0;        // flattened step over (tile, K slice), in step with the loading waves
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -269,9 +307,7 @@ void swiglu_gemm_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
     for (int kt = 0; kt < nk; ++kt, ++s) {
-      wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
       lds_barrier();       // slice s visible to all waves; slice s-1 no longer read
-      if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
       const uint16_t* As = smem + (s % GM_STAGES) * GM_STAGE_ELEMS;
       const uint16_t* Bs = As + GM_A_ELEMS;
 #pragma unroll
@@ -297,8 +333,8 @@ void swiglu_gemm_kernel(
     // 8 (r/4) + 4 (l/32) + r%4 of its 32 x 32 block, so registers 4g..4g+3 are 4
     // consecutive columns: one 8-byte store each.  N is a multiple of 64, so a
     // group of 4 is either wholly inside a partial last N tile or wholly past it.
-    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, tile_off, expert_offsets, E,
-                                   dense_M, n_tiles, out_rows);
+    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
+                                   n_tiles, out_rows);
     const int ccol = 4 * (lane >> 5);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -401,8 +437,6 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* __res
   }
 }
 
-constexpr size_t kGemmLds = size_t(GM_STAGES) * GM_STAGE_ELEMS * sizeof(uint16_t);
-
 // One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
 // a multiple of the XCD count.
 int persistent_grid() {
@@ -415,7 +449,7 @@ int persistent_grid() {
     else
       cus = 256;
   }
-  return (cus * GM_OCC + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
+  return (cus + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
 }
 
 template <bool UP>
@@ -427,11 +461,11 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&swiglu_gemm_kernel<UP>),
                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                            static_cast<int>(kGemmLds)) != hipSuccess)
+                            static_cast<int>(GM_LDS)) != hipSuccess)
       return REFLEX_ERR_LAUNCH;
     attr_set = true;
   }
-  hipLaunchKernelGGL(swiglu_gemm_kernel<UP>, dim3(persistent_grid()), dim3(GM_THREADS), kGemmLds, s,
+  hipLaunchKernelGGL(swiglu_gemm_kernel<UP>, dim3(persistent_grid()), dim3(GM_THREADS), GM_LDS, s,
                      x, gather, tile_off, eo, E, dense_M, w0, w1, stride, K, N, x_rows, out_rows,
                      packed, out);
   return launch_status();

@@ -486,12 +486,35 @@ def test_fused_edge_shapes(torch, seed, E, kmax, T):
     layer_tolerance_check(out, ref, f"edge E={E} k_max={kmax} T={T}")
 
 
-def test_one_expert_takes_every_token(torch):
-    # a huge router bias sends every token to expert 3: one expert with T rows spans many
-    # M tiles, every other expert is empty
-    w = make_fuzz_workload(200, T=2000, d=256, E=16, f=128, k_max=1)
-    w.router_bias = np.zeros(16, np.float32)
-    w.router_bias[3] = 1e4
+@pytest.mark.parametrize("seed,T,d,E,f,kmax", [(110, 1100, 256, 4, 192, 3), (111, 3000, 128, 8, 64, 4),
+                                                (112, 700, 384, 1, 128, 1)])
+def test_fused_many_rows_per_expert(torch, seed, T, d, E, f, kmax):
+    # few experts with many pairs each: every expert spans several 128-row M tiles
+    # with a ragged last one; f = 192 also leaves a partial last N tile in the up GEMM
+    w = make_fuzz_workload(seed, T=T, d=d, E=E, f=f, k_max=kmax)
+    assert w.T * w.params.k_max // w.E >= 512
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    dw = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()), "w_down": to_device(w.w_down()),
+          "w_router": to_device(w.w_router()),
+          "router_bias": None if w.router_bias is None else to_device(w.router_bias)}
+    lay = MoELayer(w.T, w.d, ExpertWeights(**dw), w.params)
+    out = oracle.bf16_to_f64(bf16_bits(lay.forward(to_device(w.h), TokenState(**state_tensors(w)))))
+    torch.cuda.synchronize()
+    k = lay.k.cpu().numpy()
+    assert np.array_equal(k, oracle_budget(w).k)
+    route = oracle.topk_route(lay.logits.cpu().numpy().astype(np.float64), k)
+    wg, wu, wd = w.w_gate(), w.w_up(), w.w_down()
+    ref = oracle.moe_layer(w.h, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
+    layer_tolerance_check(out, ref, f"many rows per expert T={T} d={d} E={E} f={f}")
+
+
+@pytest.mark.parametrize("E", [16, 2])
+def test_one_expert_takes_every_token(torch, E):
+    # a huge router bias sends every token to expert 1: one expert with T rows spans many
+    # M tiles, every other expert is empty.
+    w = make_fuzz_workload(200, T=2000, d=256, E=E, f=128, k_max=1)
+    w.router_bias = np.zeros(E, np.float32)
+    w.router_bias[1] = 1e4
     w.params = w.params.replace(k_min=1, k_max=1)
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
     dw = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()), "w_down": to_device(w.w_down()),
@@ -502,21 +525,24 @@ def test_one_expert_takes_every_token(torch):
     k = lay.k.cpu().numpy()
     assert np.all(k == 1)
     route = oracle.topk_route(lay.logits.cpu().numpy().astype(np.float64), k)
-    assert np.all(route.expert == 3)
+    assert np.all(route.expert == 1)
     wg, wu, wd = w.w_gate(), w.w_up(), w.w_down()
     ref = oracle.moe_layer(w.h, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
     layer_tolerance_check(out, ref, "one expert")
 
 
 @pytest.mark.parametrize("case", ["lladamoe_t1024_e64", "llada2mini_t4096_e256", "fuzz_d128_f64",
-                                  "fuzz_d384_f192"])
+                                  "fuzz_d384_f192", "tall_d256_f192"])
 def test_packed_weights_give_bitwise_identical_layer(torch, case):
     # the packed layout only changes where the GEMM reads each weight slice from;
     # every product and sum is the same, so the outputs must match bit for bit
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
-    if case.startswith("fuzz"):
+    if case.startswith("fuzz") or case.startswith("tall"):
         d, f = (int(x[1:]) for x in case.split("_")[1:])
-        w = make_fuzz_workload(300 + d, T=900, d=d, E=12, f=f, k_max=6)
+        if case.startswith("tall"):     # 4 experts with ~1000 rows each
+            w = make_fuzz_workload(400 + d, T=2000, d=d, E=4, f=f, k_max=2)
+        else:
+            w = make_fuzz_workload(300 + d, T=900, d=d, E=12, f=f, k_max=6)
         dv = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()),
               "w_down": to_device(w.w_down()), "w_router": to_device(w.w_router()),
               "router_bias": None if w.router_bias is None else to_device(w.router_bias)}
