@@ -27,8 +27,11 @@ struct BudgetConsts {
 
 __device__ __forceinline__ double logistic(double x) { return 1.0 / (1.0 + exp(-x)); }
 
-// Ranking key of one candidate token (hist >= 1).
-__device__ double rank_key(const BudgetConsts& p, float c1f, float c2f, int hist) {
+// Ranking key of one candidate token (hist >= 1).  Out of line: it is called from
+// several unrolled loops and would otherwise be inlined (with its three exp calls)
+// at every one of them.
+__device__ __attribute__((noinline)) double rank_key(const BudgetConsts& p, float c1f, float c2f,
+                                                   int hist) {
   const double c1 = static_cast<double>(c1f), c2 = static_cast<double>(c2f);
   const double w = p.w;
   double v_bar, c_hat;
