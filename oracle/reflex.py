@@ -33,6 +33,7 @@ __all__ = [
     "frontier_factor", "progress_factor", "frontier_progress_score", "ranking_key",
     "fger_groups", "assign_budget", "BudgetResult",
     "topk_route", "RouteResult", "pair_permutation", "PermResult",
+    "router_probs", "topp_counts", "threshold_counts",
     "swiglu_expert", "moe_layer", "dense_masked_moe", "fixed_topk_moe",
     "routed_expert_flops", "SIGNAL_FPS", "SIGNAL_FRONTIER", "SIGNAL_PROGRESS",
     "SIGNAL_CONFIDENCE", "SIGNAL_UNCERTAINTY",
@@ -275,6 +276,51 @@ def topk_route(r: np.ndarray, k: np.ndarray, norm_topk: int = 1) -> RouteResult:
         tok[lo:lo + ki] = i
         wt[lo:lo + ki] = num / den
     return RouteResult(offs, ex, tok, wt)
+
+
+# ---------------------------------------------------------------------------------------
+# score-derived count rules compared in Appendix B (Top-p, Expert-Threshold Routing)
+# ---------------------------------------------------------------------------------------
+def router_probs(r: np.ndarray) -> np.ndarray:
+    """Routing mass of every expert: the softmax of the router scores over all E
+    experts, fp64.  r: [T,E]."""
+    r = np.asarray(r, dtype=np.float64)
+    ex = np.exp(r - r.max(axis=1, keepdims=True))
+    return ex / ex.sum(axis=1, keepdims=True)
+
+
+def topp_counts(r: np.ndarray, p: float, k_min: int, k_max: int):
+    """Top-p (Appendix B): the smallest number of router-ranked experts (score
+    descending, index ascending) whose cumulative routing mass reaches p, clamped to
+    [k_min, k_max].  Returns (k, cum) where cum[i] is the cumulative mass of the
+    unclamped prefix (for margin checks)."""
+    r = np.asarray(r, dtype=np.float64)
+    T, E = r.shape
+    prob = router_probs(r)
+    pp = _p64(p)
+    k = np.zeros(T, dtype=np.int64)
+    cum_at = np.zeros(T, dtype=np.float64)
+    e_idx = np.arange(E)
+    for i in range(T):
+        order = np.lexsort((e_idx, -(r[i] + 0.0)))
+        cum = 0.0
+        n = E
+        for j, e in enumerate(order):
+            cum += prob[i, e]
+            if cum >= pp:
+                n = j + 1
+                break
+        k[i] = min(max(n, k_min), k_max)
+        cum_at[i] = cum
+    return k, cum_at
+
+
+def threshold_counts(r: np.ndarray, tau: float, k_min: int, k_max: int) -> np.ndarray:
+    """Expert-Threshold Routing (Appendix B): the number of experts whose routing mass
+    exceeds tau, clamped to [k_min, k_max]."""
+    prob = router_probs(r)
+    n = (prob > _p64(tau)).sum(axis=1)
+    return np.clip(n, k_min, k_max).astype(np.int64)
 
 
 @dataclass

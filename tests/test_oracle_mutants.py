@@ -42,6 +42,12 @@ MUTANTS = [
     ("router bias dropped", "r = r + np.asarray(bias, dtype=np.float64)[None, :]", "r = r"),
     ("bf16 rounding truncates", "r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
      "r = np.ldexp(np.trunc(np.ldexp(m, 8)), e - 8)"),
+    ("Top-p needs strictly more than p", "if cum >= pp:", "if cum > pp:"),
+    ("Top-p ranks ascending", "order = np.lexsort((e_idx, -(r[i] + 0.0)))",
+     "order = np.lexsort((e_idx, (r[i] + 0.0)))"),
+    ("threshold inclusive", "n = (prob > _p64(tau)).sum(axis=1)", "n = (prob >= _p64(tau)).sum(axis=1)"),
+    ("threshold counts unclamped", "return np.clip(n, k_min, k_max).astype(np.int64)",
+     "return n.astype(np.int64)"),
 ]
 
 
@@ -59,6 +65,7 @@ def test_pins_catch_mutant(name, old, new, source, tmp_path):
                         ignore=shutil.ignore_patterns("__pycache__", "test_oracle_mutants.py"))
     (tmp_path / "oracle" / "reflex.py").write_text(source.replace(old, new))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        "tests/test_oracle_budget.py", "tests/test_oracle_layer.py"],
+                        "tests/test_oracle_budget.py", "tests/test_oracle_layer.py",
+                        "tests/test_oracle_rules.py"],
                        cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert r.returncode != 0, f"mutant '{name}' survived the oracle pins"
