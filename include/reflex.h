@@ -148,6 +148,30 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
                          double* fps_out, void* stream);
 
 /*
+ * Counts derived from the router scores alone: the score-threshold rules the
+ * paper compares against (Appendix B).  Routing mass is the softmax of a token's
+ * scores over all E experts, evaluated in fp64.
+ *  rule = REFLEX_RULE_TOP_P:     k_i = the smallest n such that the n best experts
+ *                                (logit descending, index ascending) hold routing
+ *                                mass >= threshold (summed in that order);
+ *  rule = REFLEX_RULE_THRESHOLD: k_i = the number of experts with routing mass
+ *                                > threshold;
+ * then k_i = min(max(k_i, k_min), k_max).
+ *  logits    [T, E] fp32
+ *  threshold p in (0, 1] for Top-p; tau in [0, 1) for the threshold rule (a float,
+ *            widened exactly to fp64)
+ *  k_out     [T] int32 output counts
+ *  pairs_out [1] int32 output sum_i k_i, or NULL
+ * Errors: NULL logits / k_out; unknown rule or threshold out of range
+ * (REFLEX_ERR_PARAM); k_min < 0, k_min > k_max or k_max > min(E, 32) (REFLEX_ERR_SHAPE).
+ */
+#define REFLEX_RULE_BUDGET     0   /* Refinement-Role Budgeting + FGER (Sections 4.2-4.3) */
+#define REFLEX_RULE_TOP_P      1   /* Top-p over routing mass (Appendix B)                */
+#define REFLEX_RULE_THRESHOLD  2   /* Expert-Threshold Routing (Appendix B)               */
+int reflex_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
+                      int k_max, int32_t* k_out, int32_t* pairs_out, void* stream);
+
+/*
  * Variable-count TopK and routing weights (Section 3.2, Eq. (2)).
  * Token i keeps its min(max(k[i],0), k_max) best experts in the order (logit
  * descending, expert index ascending; -0.0 == +0.0).  Pairs are written
@@ -242,6 +266,9 @@ int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
  *   k_in != NULL   reuse counts computed earlier in the same forward (the paper
  *                  shares k_i across MoE layers, Section 3.3);
  *   uniform_k > 0  default fixed token-choice routing, k_i = uniform_k;
+ *   k_rule = REFLEX_RULE_TOP_P / REFLEX_RULE_THRESHOLD
+ *                  reflex_count_rule on this layer's scores with k_threshold and the
+ *                  bounds params.k_min, params.k_max;
  *   otherwise      reflex_assign_budget with `params` and the token state.
  * Pair capacity is T * kcap with kcap = uniform_k if uniform_k > 0, else params.k_max;
  * counts (k_in included) are clamped to [0, kcap].  `params` is validated only when
@@ -253,6 +280,8 @@ typedef struct {
   int32_t norm_topk;       /* as in reflex_topk_variable                               */
   int32_t uniform_k;       /* > 0: fixed count for every token                         */
   int32_t B;               /* number of sequences (budget path)                         */
+  int32_t k_rule;          /* REFLEX_RULE_*; 0 = the REFLEX budget                      */
+  float   k_threshold;     /* p or tau of the score-derived rules                       */
   const uint16_t *h;                         /* [T, d]                                   */
   const uint16_t *w_gate, *w_up, *w_down;    /* [E, f, d], [E, f, d], [E, d, f]          */
   const uint16_t *ws_gate, *ws_up, *ws_down; /* shared [fs, d], [fs, d], [d, fs] or NULL  */

@@ -36,7 +36,9 @@ _OUT_PTRS = ["out", "k_out", "pairs_out", "logits_out"]
 
 
 class MoeArgsC(ctypes.Structure):
-    _fields_ = ([(n, c_int32) for n in ("T", "d", "E", "f", "f_shared", "norm_topk", "uniform_k", "B")]
+    _fields_ = ([(n, c_int32) for n in ("T", "d", "E", "f", "f_shared", "norm_topk", "uniform_k", "B",
+                                        "k_rule")]
+                + [("k_threshold", ctypes.c_float)]
                 + [(n, c_void_p) for n in _ARG_PTRS]
                 + [("params", AllocParamsC)]
                 + [(n, c_void_p) for n in _OUT_PTRS])
@@ -53,6 +55,8 @@ _SIGS = {
     "reflex_router_logits": (c_int, [c_void_p] * 4 + [c_int] * 3 + [c_void_p]),
     "reflex_assign_budget": (c_int, [c_void_p] * 7 + [c_int, c_int, ctypes.POINTER(AllocParamsC)]
                              + [c_void_p] * 4),
+    "reflex_count_rule": (c_int, [c_void_p, c_int, c_int, c_int, ctypes.c_float, c_int, c_int,
+                                  c_void_p, c_void_p, c_void_p]),
     "reflex_topk_variable": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_int, c_void_p,
                                      c_void_p, c_void_p, c_int32, c_void_p]),
     "reflex_permute": (c_int, [c_void_p] * 3 + [c_int, c_int, c_int32] + [c_void_p] * 4
@@ -157,6 +161,15 @@ def reflex_assign_budget(block_idx, masked, hist_len, conf_prev1, conf_prev2, se
                                       ptr(conf_prev2), ptr(seq_offsets), ptr(active_block), B, T,
                                       ctypes.byref(prm), ptr(k_out), ptr(pairs_out), ptr(fps_out),
                                       stream_handle(stream)), "reflex_assign_budget")
+
+
+RULE_BUDGET, RULE_TOP_P, RULE_THRESHOLD = 0, 1, 2
+
+
+def reflex_count_rule(logits, rule, threshold, k_min, k_max, k_out, pairs_out=None, stream=None):
+    T, E = logits.shape
+    _check(lib().reflex_count_rule(ptr(logits), T, E, rule, threshold, k_min, k_max, ptr(k_out),
+                                   ptr(pairs_out), stream_handle(stream)), "reflex_count_rule")
 
 
 def reflex_topk_variable(logits, k, k_max, norm_topk, pair_offsets, pair_expert, pair_weight,

@@ -65,6 +65,15 @@ int check_params(const reflex_alloc_params* p) {
 }
 
 // Fused-path workspace carve-up; every region 256-byte aligned.
+// Threshold of a score-derived count rule: p in (0, 1] for Top-p, tau in [0, 1).
+int check_rule(int rule, float threshold) {
+  if (!std::isfinite(threshold)) return REFLEX_ERR_PARAM;
+  if (rule == REFLEX_RULE_TOP_P) return threshold > 0.0f && threshold <= 1.0f ? REFLEX_OK : REFLEX_ERR_PARAM;
+  if (rule == REFLEX_RULE_THRESHOLD)
+    return threshold >= 0.0f && threshold < 1.0f ? REFLEX_OK : REFLEX_ERR_PARAM;
+  return REFLEX_ERR_PARAM;
+}
+
 struct Layout {
   size_t logits, k, scalar, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
       pair_to_sorted, perm, swiglu, y, shared_act, shared_y, total;
@@ -162,6 +171,18 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
   return launch_budget(block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offsets,
                        active_block, B, T, *params, k_out, pairs_out, fps_out,
                        static_cast<hipStream_t>(stream));
+}
+
+int reflex_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
+                      int k_max, int32_t* k_out, int32_t* pairs_out, void* stream) {
+  RFX_TRY(check_ptrs({logits, k_out}, 4));
+  RFX_TRY(check_opt_ptr(pairs_out, 4));
+  RFX_TRY(check_rule(rule, threshold));
+  if (!valid_T(T) || !valid_E(E) || !valid_kmax(k_max, E) || k_min < 0 || k_min > k_max)
+    return REFLEX_ERR_SHAPE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (T == 0) return pairs_out ? launch_fill_i32(pairs_out, 0, 1, s) : REFLEX_OK;
+  return launch_count_rule(logits, T, E, rule, threshold, k_min, k_max, k_out, pairs_out, s);
 }
 
 int reflex_topk_variable(const float* logits, const int32_t* k, int T, int E, int k_max,
@@ -264,7 +285,9 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // pair capacity T * kcap: kcap = uniform_k when set (caller counts are then clamped
   // to it), else params.k_max
   int kcap;
-  const bool budget = a->k_in == nullptr && a->uniform_k <= 0;
+  const bool by_rule = a->k_in == nullptr && a->uniform_k <= 0 && a->k_rule != REFLEX_RULE_BUDGET;
+  const bool budget = a->k_in == nullptr && a->uniform_k <= 0 && !by_rule;
+  if (by_rule) RFX_TRY(check_rule(a->k_rule, a->k_threshold));
   if (a->uniform_k > 0) {
     kcap = a->uniform_k;
   } else {
@@ -309,6 +332,9 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
     if (a->uniform_k > 0) {
       RFX_TRY(launch_fill_i32(kb, a->uniform_k, T, s));
+    } else if (by_rule) {
+      RFX_TRY(launch_count_rule(logits, T, E, a->k_rule, a->k_threshold, a->params.k_min,
+                                a->params.k_max, kb, nullptr, s));
     } else {
       RFX_TRY(launch_budget(a->block_idx, a->masked, a->hist_len, a->conf_prev1, a->conf_prev2,
                             a->seq_offsets, a->active_block, a->B, T, a->params, kb, nullptr,

@@ -96,6 +96,10 @@ int launch_fill_i32(int32_t* dst, int32_t value, int n, hipStream_t s);
 int launch_count_scan(const int32_t* k, int T, int k_max, int32_t* pair_offsets,
                       int32_t* pairs_out, hipStream_t s);
 
+// Score-derived counts (REFLEX_RULE_TOP_P / REFLEX_RULE_THRESHOLD); pairs_out nullable.
+int launch_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
+                      int k_max, int32_t* k_out, int32_t* pairs_out, hipStream_t s);
+
 int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
                 hipStream_t s);

@@ -67,6 +67,81 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
 }
 
 // ------------------------------------------------------------------------------------
+// Score-derived counts (Appendix B).  One wave per token: lane l holds experts l,
+// l+64, l+128, l+192; the routing mass exp(r_e - r_max) / sum_e' exp(r_e' - r_max)
+// is evaluated in fp64.  Top-p walks the experts in TopK order (the same 64-bit keys
+// as the TopK kernel), adding their mass in that order until it reaches p; at most
+// k_max steps are needed, since longer prefixes are clamped to k_max anyway.
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__global__ __launch_bounds__(TK_WAVES * kWave) void count_rule_kernel(
+    const float* __restrict__ logits, int T, int E, int rule, double thr, int k_min, int k_max,
+    int32_t* __restrict__ k_out, int32_t* __restrict__ pairs_out) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * TK_WAVES + (threadIdx.x >> 6);
+  if (i >= T) return;
+  const float* row = logits + static_cast<size_t>(i) * E;
+  uint64_t key[4];
+  float val[4];
+  uint64_t best = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + kWave * j;
+    val[j] = e < E ? row[e] : 0.0f;
+    key[j] = e < E ? (static_cast<uint64_t>(f32_order_key(val[j])) << 32) | (0xffffu - e) : 0;
+    best = key[j] > best ? key[j] : best;
+  }
+  best = wave_max_u64(best);
+  const double rmax = static_cast<double>(f32_from_order_key(static_cast<uint32_t>(best >> 32)));
+  double ex[4];
+  double part = 0.0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    ex[j] = lane + kWave * j < E ? exp(static_cast<double>(val[j]) - rmax) : 0.0;
+    part += ex[j];
+  }
+  const double den = wave_sum_f64(part);
+  int n;
+  if (rule == REFLEX_RULE_THRESHOLD) {
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c += (lane + kWave * j < E && ex[j] / den > thr) ? 1 : 0;
+    n = wave_sum_i32(c);
+  } else {
+    n = k_max;
+    double cum = 0.0;
+    for (int j = 0; j < k_max; ++j) {
+      uint64_t b = key[0];
+#pragma unroll
+      for (int x = 1; x < 4; ++x) b = key[x] > b ? key[x] : b;
+      b = wave_max_u64(b);
+      const int e = 0xffff - static_cast<int>(b & 0xffffu);
+      const int slot = e >> 6;
+      double mine = 0.0;
+#pragma unroll
+      for (int x = 0; x < 4; ++x) mine = x == slot ? ex[x] : mine;
+      const double m = __shfl(mine, e & 63, kWave);
+      if ((e & 63) == lane) key[slot] = 0;     // consume the winner
+      cum += m / den;
+      if (cum >= thr) {
+        n = j + 1;
+        break;
+      }
+    }
+  }
+  const int k = n < k_min ? k_min : (n > k_max ? k_max : n);
+  if (lane == 0) {
+    k_out[i] = k;
+    if (pairs_out != nullptr && k != 0) atomicAdd(pairs_out, k);
+  }
+}
+
+// ------------------------------------------------------------------------------------
 // Permutation: stable counting sort of the token-major pair list by expert.
 //   1. per 1024-pair tile, an LDS histogram over experts
 //   2. one workgroup turns the [tile][expert] counts into start rows, expert-major
@@ -249,6 +324,18 @@ __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
 }
 
 }  // namespace
+
+int launch_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
+                      int k_max, int32_t* k_out, int32_t* pairs_out, hipStream_t s) {
+  if (pairs_out != nullptr) {
+    const int rc = launch_fill_i32(pairs_out, 0, 1, s);
+    if (rc != REFLEX_OK) return rc;
+  }
+  hipLaunchKernelGGL(count_rule_kernel, dim3((T + TK_WAVES - 1) / TK_WAVES), dim3(TK_WAVES * kWave),
+                     0, s, logits, T, E, rule, static_cast<double>(threshold), k_min, k_max, k_out,
+                     pairs_out);
+  return launch_status();
+}
 
 int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,

@@ -74,11 +74,14 @@ class MoELayer:
     """Holds the workspace and output buffers for repeated fused forwards of one shape."""
 
     def __init__(self, T: int, d: int, weights: ExpertWeights, params, uniform_k: int = 0,
-                 norm_topk: int = 1, device="cuda"):
+                 norm_topk: int = 1, k_rule: int = 0, k_threshold: float = 0.0, device="cuda"):
+        """k_rule: 0 = REFLEX budget; 1 = Top-p, 2 = Expert-Threshold with k_threshold
+        (counts bounded by params.k_min, params.k_max)."""
         self.T, self.d, self.w = T, d, weights
         self.params = params
         self.uniform_k = int(uniform_k)
         self.norm_topk = int(norm_topk)
+        self.k_rule, self.k_threshold = int(k_rule), float(k_threshold)
         self.kcap = self.uniform_k if self.uniform_k > 0 else int(params.k_max)
         nbytes = _lib.reflex_workspace_size(T, weights.E, d, weights.f, weights.f_shared, self.kcap)
         if nbytes == 0 and T > 0:
@@ -96,6 +99,7 @@ class MoELayer:
         a = _lib.MoeArgsC()
         a.T, a.d, a.E, a.f, a.f_shared = self.T, self.d, w.E, w.f, w.f_shared
         a.norm_topk, a.uniform_k = self.norm_topk, self.uniform_k
+        a.k_rule, a.k_threshold = self.k_rule, self.k_threshold
         P = _lib.ptr
         a.h, a.w_gate, a.w_up, a.w_down = P(h), P(w.w_gate), P(w.w_up), P(w.w_down)
         a.ws_gate, a.ws_up, a.ws_down = P(w.ws_gate), P(w.ws_up), P(w.ws_down)

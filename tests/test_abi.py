@@ -129,6 +129,21 @@ def test_topk_validation(L):
     assert f(FAKE, FAKE, 0, 8, 4, 1, FAKE, FAKE, FAKE, 0, None) == 0
 
 
+def test_count_rule_validation(L):
+    f = L.reflex_count_rule
+    assert f(None, 16, 8, 1, 0.2, 1, 4, FAKE, None, None) == -1
+    assert f(FAKE, 16, 8, 1, 0.2, 1, 4, ODD, None, None) == -2          # misaligned k_out
+    assert f(FAKE, 16, 8, 3, 0.2, 1, 4, FAKE, None, None) == -3         # unknown rule
+    assert f(FAKE, 16, 8, 0, 0.2, 1, 4, FAKE, None, None) == -3         # the budget is not a rule
+    assert f(FAKE, 16, 8, 1, 0.0, 1, 4, FAKE, None, None) == -3         # p must be > 0
+    assert f(FAKE, 16, 8, 1, 1.5, 1, 4, FAKE, None, None) == -3
+    assert f(FAKE, 16, 8, 2, 1.0, 1, 4, FAKE, None, None) == -3         # tau must be < 1
+    assert f(FAKE, 16, 8, 2, float("nan"), 1, 4, FAKE, None, None) == -3
+    assert f(FAKE, 16, 8, 1, 0.2, 5, 4, FAKE, None, None) == -2         # k_min > k_max
+    assert f(FAKE, 16, 8, 1, 0.2, 1, 9, FAKE, None, None) == -2         # k_max > E
+    assert f(FAKE, 0, 8, 2, 0.02, 1, 4, FAKE, None, None) == 0
+
+
 def test_permute_swiglu_combine_validation(L):
     cap, E, f_ = 64, 8, 128
     need = L.reflex_permute_workspace_size(cap, E)
