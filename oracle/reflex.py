@@ -31,7 +31,7 @@ __all__ = [
     "bf16_to_f64", "f64_to_bf16_bits", "sigmoid",
     "router_scores", "block_distance", "role_budget", "confidence_forecast",
     "frontier_factor", "progress_factor", "frontier_progress_score", "ranking_key",
-    "fger_groups", "assign_budget", "BudgetResult",
+    "fger_groups", "assign_budget", "BudgetResult", "advance_state", "StateResult",
     "topk_route", "RouteResult", "pair_permutation", "PermResult",
     "router_probs", "topp_counts", "threshold_counts",
     "swiglu_expert", "moe_layer", "dense_masked_moe", "fixed_topk_moe",
@@ -232,6 +232,65 @@ def assign_budget(block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offse
     k_unclamped = k.copy()
     k = np.minimum(np.maximum(k, p.k_min), p.k_max)
     return BudgetResult(k, k_unclamped, k_rrb, score, group, ranked)
+
+
+# ---------------------------------------------------------------------------------------
+# decoding state between denoising forwards (Section 3.1, Eq. (1))
+# ---------------------------------------------------------------------------------------
+@dataclass
+class StateResult:
+    masked: np.ndarray        # [T] uint8
+    hist_len: np.ndarray      # [T] int8
+    conf_prev1: np.ndarray    # [T] float32, c^{t} after the update (the new c^{t-1})
+    conf_prev2: np.ndarray    # [T] float32
+    active_block: np.ndarray  # [B] int32
+    committed: np.ndarray     # [T] bool, positions committed by this forward
+    remaining: np.ndarray     # [B] masked positions left in each sequence
+
+
+def advance_state(block_idx, masked, hist_len, conf_prev1, conf_prev2, seq_offsets,
+                  active_block, conf_t, theta: float, min_commit: int = 0) -> StateResult:
+    """One forward's commitment and bookkeeping, per sequence.
+
+    Confidence-threshold commitment (Eq. (1)): the committed set is the masked
+    positions of the active block whose confidence reaches theta.  With
+    min_commit = 1, a forward that would commit nothing commits the single most
+    confident such position instead (lowest position on ties), a common guard
+    for progress that the paper does not state.  Every position that was masked
+    when the forward ran records its new confidence: c^{t-2} <- c^{t-1},
+    c^{t-1} <- c^t, history length capped at 2.  When no masked position is left
+    in the active block, the sequence moves to the next block (if any)."""
+    b = np.asarray(block_idx, dtype=np.int64)
+    m = np.asarray(masked).astype(np.uint8).copy()
+    h = np.asarray(hist_len).astype(np.int8).copy()
+    c1 = np.asarray(conf_prev1, dtype=np.float32).copy()
+    c2 = np.asarray(conf_prev2, dtype=np.float32).copy()
+    ct = np.asarray(conf_t, dtype=np.float32)
+    a = np.asarray(active_block, dtype=np.int32).copy()
+    th = np.float32(theta)
+    T = len(b)
+    committed = np.zeros(T, dtype=bool)
+    remaining = np.zeros(len(a), dtype=np.int64)
+    for s in range(len(a)):
+        lo, hi = int(seq_offsets[s]), int(seq_offsets[s + 1])
+        idx = np.arange(lo, hi)
+        was_masked = idx[m[lo:hi] == 1]
+        J = was_masked[b[was_masked] == a[s]]
+        C = J[ct[J] >= th]
+        if min_commit and len(C) == 0 and len(J) > 0:
+            best = J[np.lexsort((J, -ct[J].astype(np.float64)))[0]]
+            C = np.array([best])
+        c2[was_masked] = c1[was_masked]
+        c1[was_masked] = ct[was_masked]
+        h[was_masked] = np.minimum(h[was_masked].astype(np.int64) + 1, 2).astype(np.int8)
+        m[C] = 0
+        committed[C] = True
+        last_block = int(b[lo:hi].max()) if hi > lo else int(a[s])
+        left_in_active = int(((m[lo:hi] == 1) & (b[lo:hi] == a[s])).sum())
+        if left_in_active == 0 and a[s] < last_block:
+            a[s] += 1
+        remaining[s] = int(m[lo:hi].sum())
+    return StateResult(m, h, c1, c2, a, committed, remaining)
 
 
 # ---------------------------------------------------------------------------------------

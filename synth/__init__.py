@@ -15,3 +15,4 @@ from .workloads import (  # noqa: F401
     make_fuzz_workload,
     WORKLOAD_NAMES,
 )
+from .trajectory import forward_confidence, generation_start  # noqa: F401

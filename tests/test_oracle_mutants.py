@@ -48,6 +48,12 @@ MUTANTS = [
     ("threshold inclusive", "n = (prob > _p64(tau)).sum(axis=1)", "n = (prob >= _p64(tau)).sum(axis=1)"),
     ("threshold counts unclamped", "return np.clip(n, k_min, k_max).astype(np.int64)",
      "return n.astype(np.int64)"),
+    ("commit strictly above theta", "C = J[ct[J] >= th]", "C = J[ct[J] > th]"),
+    ("history not shifted", "c2[was_masked] = c1[was_masked]", "c2[was_masked] = c2[was_masked]"),
+    ("block advances with tokens left", "if left_in_active == 0 and a[s] < last_block:",
+     "if a[s] < last_block:"),
+    ("progress guard ties to higher position", "best = J[np.lexsort((J, -ct[J].astype(np.float64)))[0]]",
+     "best = J[np.lexsort((-J, -ct[J].astype(np.float64)))[0]]"),
 ]
 
 
@@ -66,6 +72,6 @@ def test_pins_catch_mutant(name, old, new, source, tmp_path):
     (tmp_path / "oracle" / "reflex.py").write_text(source.replace(old, new))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         "tests/test_oracle_budget.py", "tests/test_oracle_layer.py",
-                        "tests/test_oracle_rules.py"],
+                        "tests/test_oracle_rules.py", "tests/test_oracle_state.py"],
                        cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert r.returncode != 0, f"mutant '{name}' survived the oracle pins"
