@@ -316,6 +316,42 @@ def cpu_baseline(w, host, seconds):
             "seconds": round(t_route + t_exp, 2)}
 
 
+def trajectory_stats(a, torch):
+    """Decode a whole synthetic generation (every block, from all-masked) with the fused
+    layer and the state kernel; report forwards (NFE), pairs and AvgK next to fixed
+    top-K_base routing over the same forwards."""
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    from paper_2608_01784_amd.trajectory import run_trajectory
+    from synth import forward_confidence, generation_start, make_workload
+    from synth.device import to_device
+    w = make_workload(a.workload, seed=a.seed)
+    if w.n_layers != 1:
+        raise SystemExit("--trajectory runs single-layer workloads")
+    dv = {k: to_device(getattr(w, k)(0)) for k in ("w_gate", "w_up", "w_down", "w_router")}
+    dv["router_bias"] = None if w.router_bias is None else to_device(w.router_bias)
+    sh = w.shared_weights(0)
+    if sh is not None:
+        dv["ws_gate"], dv["ws_up"], dv["ws_down"] = (to_device(x) for x in sh)
+    lay = MoELayer(w.T, w.d, ExpertWeights(**dv), w.params)
+    st = TokenState(**{k: to_device(v) for k, v in generation_start(w).items()})
+    h = to_device(w.h)
+    confs = [to_device(forward_confidence(a.seed, t, w.T)) for t in range(64)]
+    t0 = time.perf_counter()
+    stats = run_trajectory(lay, h, st, lambda t: confs[t] if t < len(confs) else
+                           to_device(forward_confidence(a.seed, t, w.T)), theta=w.params.theta)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    P = stats.total_pairs
+    print(json.dumps({"trajectory": {
+        "workload": w.name, "data": "synthetic confidences (seeded, rising per forward)",
+        "forwards": stats.forwards, "total_pairs": P,
+        "avg_k": round(P / (stats.forwards * w.T), 4),
+        "uniform_pairs": stats.forwards * w.T * w.params.k_base,
+        "pair_ratio_vs_uniform": round(P / (stats.forwards * w.T * w.params.k_base), 4),
+        "alloc_tflop": round(6 * w.d * w.f * P / 1e12, 3),
+        "wall_s": round(wall, 3), "pairs_per_forward": stats.pairs}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -328,6 +364,9 @@ def main():
     ap.add_argument("--no-uniform", action="store_true")
     ap.add_argument("--packed-weights", action="store_true",
                     help="pack the expert weights once (reflex_pack_*) and stream the packed layout")
+    ap.add_argument("--trajectory", action="store_true",
+                    help="run a synthetic multi-forward decoding trajectory (all blocks, from an "
+                         "all-masked start) and print its forward and pair statistics instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only the plain 256 MiB device copy that calibrates the byte counters")
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -357,6 +396,9 @@ def main():
         copy_calibration()
         return
     _lib.lib()
+    if a.trajectory:
+        trajectory_stats(a, torch)
+        return
     log(f"generating {a.workload} (seed {a.seed})")
     w = make_workload(a.workload, seed=a.seed)
     hosts, dws = [], []

@@ -148,6 +148,27 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
                          double* fps_out, void* stream);
 
 /*
+ * Decoding state after one denoising forward (Section 3.1, Eq. (1)), per sequence:
+ * the masked positions of the active block whose confidence reaches theta are
+ * committed (with min_commit = 1, a forward that would commit none commits the
+ * most confident one, lowest position on ties); every position that was masked
+ * records the forward's confidence (conf_prev2 <- conf_prev1, conf_prev1 <- conf_t,
+ * hist_len <- min(hist_len + 1, 2)); a sequence whose active block has no masked
+ * position left moves to its next block, if it has one.
+ *  conf_t       [T] fp32  confidences of this forward (read at masked positions)
+ *  block_idx    [T] int32, seq_offsets [B+1] int32   as in reflex_assign_budget
+ *  theta        commitment threshold in (0, 1]
+ *  masked, hist_len, conf_prev1, conf_prev2 [T], active_block [B]   updated in place
+ *  remaining    [B] int32 output: masked positions left per sequence, or NULL
+ * Errors: NULL required pointers; T > 0 with B < 1; theta outside (0, 1] or
+ * min_commit not 0/1 (REFLEX_ERR_PARAM).
+ */
+int reflex_advance_state(const float* conf_t, const int32_t* block_idx, const int32_t* seq_offsets,
+                         int B, int T, float theta, int min_commit, uint8_t* masked,
+                         int8_t* hist_len, float* conf_prev1, float* conf_prev2,
+                         int32_t* active_block, int32_t* remaining, void* stream);
+
+/*
  * Counts derived from the router scores alone: the score-threshold rules the
  * paper compares against (Appendix B).  Routing mass is the softmax of a token's
  * scores over all E experts, evaluated in fp64.

@@ -55,6 +55,8 @@ _SIGS = {
     "reflex_router_logits": (c_int, [c_void_p] * 4 + [c_int] * 3 + [c_void_p]),
     "reflex_assign_budget": (c_int, [c_void_p] * 7 + [c_int, c_int, ctypes.POINTER(AllocParamsC)]
                              + [c_void_p] * 4),
+    "reflex_advance_state": (c_int, [c_void_p] * 3 + [c_int, c_int, ctypes.c_float, c_int]
+                             + [c_void_p] * 7),
     "reflex_count_rule": (c_int, [c_void_p, c_int, c_int, c_int, ctypes.c_float, c_int, c_int,
                                   c_void_p, c_void_p, c_void_p]),
     "reflex_topk_variable": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_int, c_void_p,
@@ -161,6 +163,16 @@ def reflex_assign_budget(block_idx, masked, hist_len, conf_prev1, conf_prev2, se
                                       ptr(conf_prev2), ptr(seq_offsets), ptr(active_block), B, T,
                                       ctypes.byref(prm), ptr(k_out), ptr(pairs_out), ptr(fps_out),
                                       stream_handle(stream)), "reflex_assign_budget")
+
+
+def reflex_advance_state(conf_t, block_idx, seq_offsets, theta, min_commit, masked, hist_len,
+                         conf_prev1, conf_prev2, active_block, remaining=None, stream=None):
+    T = block_idx.shape[0]
+    B = active_block.shape[0]
+    _check(lib().reflex_advance_state(ptr(conf_t), ptr(block_idx), ptr(seq_offsets), B, T, theta,
+                                      min_commit, ptr(masked), ptr(hist_len), ptr(conf_prev1),
+                                      ptr(conf_prev2), ptr(active_block), ptr(remaining),
+                                      stream_handle(stream)), "reflex_advance_state")
 
 
 RULE_BUDGET, RULE_TOP_P, RULE_THRESHOLD = 0, 1, 2

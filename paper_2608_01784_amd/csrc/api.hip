@@ -173,6 +173,22 @@ int reflex_assign_budget(const int32_t* block_idx, const uint8_t* masked, const 
                        static_cast<hipStream_t>(stream));
 }
 
+int reflex_advance_state(const float* conf_t, const int32_t* block_idx, const int32_t* seq_offsets,
+                         int B, int T, float theta, int min_commit, uint8_t* masked,
+                         int8_t* hist_len, float* conf_prev1, float* conf_prev2,
+                         int32_t* active_block, int32_t* remaining, void* stream) {
+  RFX_TRY(check_ptrs({masked, hist_len}, 1));
+  RFX_TRY(check_ptrs({conf_t, block_idx, seq_offsets, conf_prev1, conf_prev2, active_block}, 4));
+  RFX_TRY(check_opt_ptr(remaining, 4));
+  if (!valid_T(T) || B < 0 || B > REFLEX_MAX_TOKENS || (T > 0 && B < 1)) return REFLEX_ERR_SHAPE;
+  if (!(theta > 0.0f && theta <= 1.0f) || (min_commit != 0 && min_commit != 1))
+    return REFLEX_ERR_PARAM;
+  if (B == 0) return REFLEX_OK;
+  return launch_advance_state(conf_t, block_idx, seq_offsets, B, T, theta, min_commit, masked,
+                              hist_len, conf_prev1, conf_prev2, active_block, remaining,
+                              static_cast<hipStream_t>(stream));
+}
+
 int reflex_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
                       int k_max, int32_t* k_out, int32_t* pairs_out, void* stream) {
   RFX_TRY(check_ptrs({logits, k_out}, 4));

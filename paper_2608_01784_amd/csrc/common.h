@@ -93,6 +93,12 @@ int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t*
 
 int launch_fill_i32(int32_t* dst, int32_t value, int n, hipStream_t s);
 
+// One forward's commitment and state bookkeeping, one workgroup per sequence.
+int launch_advance_state(const float* conf_t, const int32_t* block_idx, const int32_t* seq_offsets,
+                         int B, int T, float theta, int min_commit, uint8_t* masked,
+                         int8_t* hist_len, float* c1, float* c2, int32_t* active_block,
+                         int32_t* remaining, hipStream_t s);
+
 int launch_count_scan(const int32_t* k, int T, int k_max, int32_t* pair_offsets,
                       int32_t* pairs_out, hipStream_t s);
 

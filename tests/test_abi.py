@@ -129,6 +129,17 @@ def test_topk_validation(L):
     assert f(FAKE, FAKE, 0, 8, 4, 1, FAKE, FAKE, FAKE, 0, None) == 0
 
 
+def test_advance_state_validation(L):
+    f = L.reflex_advance_state
+    assert f(None, FAKE, FAKE, 1, 16, 0.9, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert f(FAKE, FAKE, FAKE, 1, 16, 0.9, 0, FAKE, FAKE, ODD, FAKE, FAKE, None, None) == -2
+    assert f(FAKE, FAKE, FAKE, 0, 16, 0.9, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -2  # B < 1
+    assert f(FAKE, FAKE, FAKE, 1, 16, 0.0, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -3  # theta
+    assert f(FAKE, FAKE, FAKE, 1, 16, 1.5, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -3
+    assert f(FAKE, FAKE, FAKE, 1, 16, 0.9, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == -3  # min_commit
+    assert f(FAKE, FAKE, FAKE, 0, 0, 0.9, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 0
+
+
 def test_count_rule_validation(L):
     f = L.reflex_count_rule
     assert f(None, 16, 8, 1, 0.2, 1, 4, FAKE, None, None) == -1
