@@ -89,6 +89,28 @@ typedef struct {
   int32_t signal;      /* REFLEX_SIGNAL_*                                           */
 } reflex_alloc_params;
 
+/*
+ * The paper's settings as ready-made parameters (host only, no GPU work):
+ * Section 5.1 defaults with the given count bounds and frontier width, and the
+ * ablation variants of Section 5.3 and Appendix C:
+ *  REFLEX_PRESET_FULL         RRB + FGER with the Frontier-Progress Score
+ *  REFLEX_PRESET_RRB_ONLY     delta_cur = 0 (no reallocation inside the active block)
+ *  REFLEX_PRESET_FGER_ONLY    delta_role = 0 (every role keeps k_base)
+ *  REFLEX_PRESET_FRONTIER_ONLY, _PROGRESS_ONLY, _CONFIDENCE_ONLY, _UNCERTAINTY_ONLY
+ *                             the full method ranking by one signal (REFLEX_SIGNAL_*)
+ *  k_min, k_max   count bounds (e.g. 2, 12); w_cf 0.30 (LLaDA-MoE) or 0.25 (LLaDA2.0-mini)
+ * Errors: NULL out; unknown preset (REFLEX_ERR_PARAM); the result failing the
+ * validity rules above (REFLEX_ERR_PARAM).
+ */
+#define REFLEX_PRESET_FULL              0
+#define REFLEX_PRESET_RRB_ONLY          1
+#define REFLEX_PRESET_FGER_ONLY         2
+#define REFLEX_PRESET_FRONTIER_ONLY     3
+#define REFLEX_PRESET_PROGRESS_ONLY     4
+#define REFLEX_PRESET_CONFIDENCE_ONLY   5
+#define REFLEX_PRESET_UNCERTAINTY_ONLY  6
+int reflex_alloc_preset(int preset, int k_min, int k_max, float w_cf, reflex_alloc_params* out);
+
 /* ---- introspection ---------------------------------------------------------- */
 int         reflex_version(void);               /* 100 * major + minor                */
 const char* reflex_status_string(int status);   /* static string, never NULL          */

@@ -55,6 +55,7 @@ _SIGS = {
     "reflex_router_logits": (c_int, [c_void_p] * 4 + [c_int] * 3 + [c_void_p]),
     "reflex_assign_budget": (c_int, [c_void_p] * 7 + [c_int, c_int, ctypes.POINTER(AllocParamsC)]
                              + [c_void_p] * 4),
+    "reflex_alloc_preset": (c_int, [c_int, c_int, c_int, ctypes.c_float, ctypes.POINTER(AllocParamsC)]),
     "reflex_advance_state": (c_int, [c_void_p] * 3 + [c_int, c_int, ctypes.c_float, c_int]
                              + [c_void_p] * 7),
     "reflex_count_rule": (c_int, [c_void_p, c_int, c_int, c_int, ctypes.c_float, c_int, c_int,
@@ -176,6 +177,17 @@ def reflex_advance_state(conf_t, block_idx, seq_offsets, theta, min_commit, mask
 
 
 RULE_BUDGET, RULE_TOP_P, RULE_THRESHOLD = 0, 1, 2
+PRESETS = ("full", "rrb_only", "fger_only", "frontier_only", "progress_only", "confidence_only",
+           "uncertainty_only")
+
+
+def reflex_alloc_preset(preset, k_min, k_max, w_cf) -> AllocParamsC:
+    """The paper's hyper-parameters for a named or numbered preset (host only)."""
+    idx = PRESETS.index(preset) if isinstance(preset, str) else int(preset)
+    out = AllocParamsC()
+    _check(lib().reflex_alloc_preset(idx, k_min, k_max, w_cf, ctypes.byref(out)),
+           "reflex_alloc_preset")
+    return out
 
 
 def reflex_count_rule(logits, rule, threshold, k_min, k_max, k_out, pairs_out=None, stream=None):

@@ -129,6 +129,35 @@ const char* reflex_status_string(int status) {
 }
 
 size_t reflex_sizeof_alloc_params(void) { return sizeof(reflex_alloc_params); }
+
+int reflex_alloc_preset(int preset, int k_min, int k_max, float w_cf, reflex_alloc_params* out) {
+  if (out == nullptr) return REFLEX_ERR_NULL;
+  if (preset < REFLEX_PRESET_FULL || preset > REFLEX_PRESET_UNCERTAINTY_ONLY) return REFLEX_ERR_PARAM;
+  reflex_alloc_params p;
+  p.k_base = 8;          // Section 5.1
+  p.delta_role = 4;
+  p.delta_cur = 2;
+  p.k_min = k_min;
+  p.k_max = k_max;
+  p.q = 0.25f;
+  p.theta = 0.9f;
+  p.w_cf = w_cf;
+  p.v_ref = 0.01f;
+  p.tau = 0.05f;
+  p.signal = REFLEX_SIGNAL_FPS;
+  switch (preset) {
+    case REFLEX_PRESET_RRB_ONLY: p.delta_cur = 0; break;
+    case REFLEX_PRESET_FGER_ONLY: p.delta_role = 0; break;
+    case REFLEX_PRESET_FRONTIER_ONLY: p.signal = REFLEX_SIGNAL_FRONTIER; break;
+    case REFLEX_PRESET_PROGRESS_ONLY: p.signal = REFLEX_SIGNAL_PROGRESS; break;
+    case REFLEX_PRESET_CONFIDENCE_ONLY: p.signal = REFLEX_SIGNAL_CONFIDENCE; break;
+    case REFLEX_PRESET_UNCERTAINTY_ONLY: p.signal = REFLEX_SIGNAL_UNCERTAINTY; break;
+    default: break;
+  }
+  RFX_TRY(check_params(&p));
+  *out = p;
+  return REFLEX_OK;
+}
 size_t reflex_sizeof_moe_args(void) { return sizeof(reflex_moe_args); }
 
 size_t reflex_workspace_size(int T, int E, int d, int f, int f_shared, int k_max) {

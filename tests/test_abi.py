@@ -6,6 +6,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 from conftest import ROOT
@@ -127,6 +128,32 @@ def test_topk_validation(L):
     assert f(FAKE, FAKE, 16, 8, 4, 2, FAKE, FAKE, FAKE, 64, None) == -3      # norm_topk
     assert f(FAKE, FAKE, 16, 8, 4, 1, FAKE, FAKE, FAKE, 63, None) == -4      # capacity < T k_max
     assert f(FAKE, FAKE, 0, 8, 4, 1, FAKE, FAKE, FAKE, 0, None) == 0
+
+
+@pytest.mark.parametrize("preset,field,value", [
+    ("full", None, None), ("rrb_only", "delta_cur", 0), ("fger_only", "delta_role", 0),
+    ("frontier_only", "signal", 1), ("progress_only", "signal", 2), ("confidence_only", "signal", 3),
+    ("uncertainty_only", "signal", 4)])
+def test_alloc_presets_hold_the_paper_settings(L, preset, field, value):
+    # Section 5.1: K_base 8, delta_role 4, delta_cur 2, q 0.25, theta 0.9, v_ref 0.01, tau 0.05
+    from paper_2608_01784_amd import _lib
+    p = _lib.reflex_alloc_preset(preset, 2, 12, 0.30)
+    expect = {"k_base": 8, "delta_role": 4, "delta_cur": 2, "k_min": 2, "k_max": 12, "signal": 0}
+    if field is not None:
+        expect[field] = value
+    for k, v in expect.items():
+        assert getattr(p, k) == v, k
+    f32 = lambda x: float(np.float32(x))  # noqa: E731
+    assert (p.q, p.theta, p.w_cf, p.v_ref, p.tau) == (0.25, f32(0.9), f32(0.30), f32(0.01), f32(0.05))
+
+
+def test_alloc_preset_validation(L):
+    from paper_2608_01784_amd import _lib
+    out = _lib.AllocParamsC()
+    assert L.reflex_alloc_preset(7, 2, 12, 0.3, ctypes.byref(out)) == -3
+    assert L.reflex_alloc_preset(0, 2, 12, 0.3, None) == -1
+    assert L.reflex_alloc_preset(0, 13, 12, 0.3, ctypes.byref(out)) == -3
+    assert L.reflex_alloc_preset(0, 2, 12, 0.0, ctypes.byref(out)) == -3     # w_cf > 0
 
 
 def test_advance_state_validation(L):

@@ -137,6 +137,22 @@ def test_budget_ranking_signals(torch, name, signal):
     check_budget(torch, w, w.params.replace(signal=signal))
 
 
+@pytest.mark.parametrize("preset", ["full", "rrb_only", "fger_only", "frontier_only",
+                                    "progress_only", "confidence_only", "uncertainty_only"])
+@pytest.mark.parametrize("name", ["lladamoe_t1024_e64", "llada2mini_t4096_e256", "fuzz5"])
+def test_budget_paper_presets(torch, name, preset):
+    # the library's presets, converted to the oracle's parameters field by field
+    w = workload(name)
+    c = _lib().reflex_alloc_preset(preset, w.params.k_min, w.params.k_max, w.params.w_cf)
+    p = AllocParams.make(c.k_base, c.delta_role, c.delta_cur, c.k_min, c.k_max, q=c.q,
+                         theta=c.theta, w_cf=c.w_cf, v_ref=c.v_ref, tau=c.tau).replace(signal=c.signal)
+    k, ref = check_budget(torch, w, p)
+    if preset == "rrb_only":          # no reallocation: the clamped role budget
+        assert np.array_equal(k, np.clip(ref.k_rrb, p.k_min, p.k_max))
+    if preset == "fger_only" and p.k_max >= 10 and p.k_min <= 6:
+        assert int(k.sum()) == 8 * w.T            # FGER alone preserves the budget
+
+
 @pytest.mark.parametrize("active", [1, 2, 3, 9, 15, 16])
 def test_budget_every_role_position(torch, active):
     check_budget(torch, make_workload("lladamoe_t1024_e64", active=active))

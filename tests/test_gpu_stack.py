@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 from gpu_common import layer_tolerance_check, note, oracle_budget, require_gpu
-from synth import make_workload
+from synth import make_fuzz_workload, make_workload
 from synth.device import bf16_bits, state_tensors, to_device
 
 pytestmark = pytest.mark.gpu
@@ -78,3 +78,37 @@ def test_stack16_teacher_forced(torch):
     # end-to-end drift is reported, not asserted: the stack compounds 16 roundings
     h_last = oracle.bf16_to_f64(bf16_bits(h[L])[toks])
     note(f"{NAME}: |h_16| rms {np.sqrt((h_last ** 2).mean()):.3f}")
+
+
+def test_per_layer_counts(torch):
+    # counts given per layer as rows of an [L, T] array (a per-layer allocation,
+    # Section 3.3's generalisation); each layer is checked against the oracle with
+    # its own row, teacher forced
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer
+    w = make_fuzz_workload(321, T=700, d=256, E=16, f=128, k_max=6)
+    L = 3
+    k_rows = np.random.default_rng(9).integers(0, w.params.k_max + 1, (L, w.T)).astype(np.int32)
+    k_dev = to_device(k_rows)
+    lay = None
+    h = [to_device(w.h)]
+    logits = []
+    res = [to_device(w.residual(l)) for l in range(L)]
+    for l in range(L):
+        ew = ExpertWeights(w_gate=to_device(w.w_gate(l)), w_up=to_device(w.w_up(l)),
+                           w_down=to_device(w.w_down(l)), w_router=to_device(w.w_router(l)))
+        if lay is None:
+            lay = MoELayer(w.T, w.d, ew, w.params)
+        lay.w = ew
+        out = torch.empty_like(h[0])
+        lay.forward(h[l], k_in=k_dev[l], residual_a=h[l], residual_b=res[l], out=out)
+        assert int(lay.pairs.item()) == int(k_rows[l].sum())
+        logits.append(lay.logits.cpu().numpy().astype(np.float64))
+        h.append(out)
+    torch.cuda.synchronize()
+    for l in range(L):
+        h_in = bf16_bits(h[l])
+        route = oracle.topk_route(logits[l], k_rows[l])
+        wg, wu, wd = w.w_gate(l), w.w_up(l), w.w_down(l)
+        ref = (oracle.moe_layer(h_in, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
+               + oracle.bf16_to_f64(h_in) + oracle.bf16_to_f64(w.residual(l)))
+        layer_tolerance_check(oracle.bf16_to_f64(bf16_bits(h[l + 1])), ref, f"per-layer counts, layer {l}")
