@@ -352,7 +352,8 @@ int reflex_moe_forward(const reflex_moe_args* args, void* ws, size_t ws_bytes, v
 /*
  * reflex_moe_forward with timing marks, for benchmarks: identical work, plus
  * hipEventRecord(stage_events[i], stream) at each stage boundary:
- *   0 start, 1 router done, 2 counts done (budget / uniform fill / reuse),
+ *   0 start, 1 router done (for layers with T < 4096 the REFLEX counts are
+ *   computed in the same launch), 2 counts done (budget / rule / uniform fill / reuse),
  *   3 count scan + TopK done, 4 permutation + GEMM tile plan done,
  *   5 gate/up GEMM done, 6 down GEMM done, 7 shared expert done, 8 combine done.
  * stage_events: host array of REFLEX_N_STAGE_EVENTS hipEvent_t handles created by

@@ -370,9 +370,19 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   void* gws = at(L.swiglu);
 
   RFX_TRY(mark(0));
-  RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s));
-  RFX_TRY(mark(1));
   const int32_t* k = a->k_in;
+  // small layers: scores and counts in one launch (independent work side by side)
+  const bool front = budget && front_fits(T, d);
+  if (front) {
+    int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
+    RFX_TRY(launch_front(a->h, a->w_router, a->router_bias, logits, T, d, E, a->block_idx, a->masked,
+                         a->hist_len, a->conf_prev1, a->conf_prev2, a->seq_offsets, a->active_block,
+                         a->B, a->params, kb, s));
+    k = kb;
+  } else {
+    RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s));
+  }
+  RFX_TRY(mark(1));
   if (k == nullptr) {
     int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
     if (a->uniform_k > 0) {

@@ -93,6 +93,14 @@ int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t*
 
 int launch_fill_i32(int32_t* dst, int32_t value, int n, hipStream_t s);
 
+// Router scores and REFLEX counts in one launch; only for shapes where front_fits().
+bool front_fits(int T, int d);
+int launch_front(const uint16_t* h, const float* w, const float* bias, float* logits, int T, int d,
+                 int E, const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
+                 const float* c1, const float* c2, const int32_t* seq_offsets,
+                 const int32_t* active_block, int B, const reflex_alloc_params& p, int32_t* k_out,
+                 hipStream_t s);
+
 // One forward's commitment and state bookkeeping, one workgroup per sequence.
 int launch_advance_state(const float* conf_t, const int32_t* block_idx, const int32_t* seq_offsets,
                          int B, int T, float theta, int min_commit, uint8_t* masked,
