@@ -323,6 +323,110 @@ __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
   }
 }
 
+// Small pair lists (capacity <= PS_MAX_CAP): the whole permutation in one
+// 1024-thread workgroup, with every pair's owning token in an LDS table: LDS
+// histogram, expert scan (+ GEMM tile plan), then 1024-pair steps ranked exactly as
+// in the per-tile scatter above, carrying each expert's running row across steps.
+// Saves two launches and their gaps where the list is short.
+constexpr int PS_THREADS = 1024;
+constexpr int PS_WAVES = PS_THREADS / kWave;
+constexpr int PS_MAX_CAP = 16384;
+
+__global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
+    const int32_t* __restrict__ pair_offsets, const int32_t* __restrict__ pair_expert,
+    const int32_t* __restrict__ pairs, int T, int cap, int E, int32_t* __restrict__ expert_offsets,
+    int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted,
+    int32_t* __restrict__ gemm_tile_off) {
+  __shared__ int owner[PS_MAX_CAP];
+  __shared__ uint8_t pexp[PS_MAX_CAP];           // each pair's expert (E <= 256)
+  __shared__ int cnt[REFLEX_MAX_EXPERTS], run[REFLEX_MAX_EXPERTS];
+  __shared__ int wcnt[PS_WAVES][REFLEX_MAX_EXPERTS];
+  __shared__ int s_wave[8];
+  const int P = pair_count(pairs, cap);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  for (int x = tid; x < PS_WAVES * REFLEX_MAX_EXPERTS; x += PS_THREADS) (&wcnt[0][0])[x] = 0;
+  for (int e = tid; e < REFLEX_MAX_EXPERTS; e += PS_THREADS) cnt[e] = 0;
+  __syncthreads();
+  for (int t = tid; t < T; t += PS_THREADS) {
+    const int p0 = max(pair_offsets[t], 0), p1 = min(pair_offsets[t + 1], P);
+    for (int p = p0; p < p1; ++p) owner[p] = t;
+  }
+  for (int p = tid; p < P; p += PS_THREADS) {
+    int e = pair_expert[p];
+    e = e < 0 ? 0 : (e >= E ? E - 1 : e);
+    pexp[p] = static_cast<uint8_t>(e);
+    atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  // expert scan (waves 0..3, one expert per thread) and the GEMM's M-tile prefix
+  int n = 0, incl = 0, tiles = 0, tincl = 0;
+  if (tid < REFLEX_MAX_EXPERTS) {
+    n = tid < E ? cnt[tid] : 0;
+    tiles = (n + kGemmBM - 1) / kGemmBM;
+    incl = wave_inclusive_scan_i32(n, lane);
+    tincl = wave_inclusive_scan_i32(tiles, lane);
+    if (lane == 63) {
+      s_wave[wv] = incl;
+      s_wave[4 + wv] = tincl;
+    }
+  }
+  __syncthreads();
+  if (tid < E) {
+    int off = 0, toff = 0;
+    for (int x = 0; x < wv; ++x) {
+      off += s_wave[x];
+      toff += s_wave[4 + x];
+    }
+    const int base = off + incl - n;
+    run[tid] = base;
+    expert_offsets[tid] = base;
+    if (tid == E - 1) expert_offsets[E] = base + n;
+    if (gemm_tile_off != nullptr) {
+      gemm_tile_off[tid] = toff + tincl - tiles;
+      if (tid == E - 1) gemm_tile_off[E] = toff + tincl;
+    }
+  }
+  __syncthreads();
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  for (int c = 0; c < P; c += PS_THREADS) {      // uniform across the workgroup
+    const int p = c + tid;
+    const bool valid = p < P;
+    int e = 0, tok = 0;
+    if (valid) {
+      e = pexp[p];
+      tok = owner[p];
+    }
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (e >> b) & 1;
+      const uint64_t m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    const int local = __popcll(same & lt_mask);
+    if (valid && local == 0) wcnt[wv][e] = __popcll(same);
+    __syncthreads();
+    if (valid) {
+      int pos = run[e] + local;
+#pragma unroll
+      for (int w = 0; w < PS_WAVES; ++w) pos += w < wv ? wcnt[w][e] : 0;
+      sorted_token[pos] = tok;
+      pair_to_sorted[p] = pos;
+    }
+    __syncthreads();
+    for (int x = tid; x < E; x += PS_THREADS) {
+      int add = 0;
+#pragma unroll
+      for (int w = 0; w < PS_WAVES; ++w) {
+        add += wcnt[w][x];
+        wcnt[w][x] = 0;
+      }
+      run[x] += add;
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
 int launch_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
@@ -354,6 +458,11 @@ size_t permute_ws_bytes(int pair_capacity, int E) {
 int launch_permute(const int32_t* pair_offsets, const int32_t* pair_expert, const int32_t* pairs,
                    int T, int E, int cap, int32_t* expert_offsets, int32_t* sorted_token,
                    int32_t* pair_to_sorted, void* ws, int32_t* gemm_tile_off, hipStream_t s) {
+  if (cap <= PS_MAX_CAP) {
+    hipLaunchKernelGGL(perm_small_kernel, dim3(1), dim3(PS_THREADS), 0, s, pair_offsets, pair_expert,
+                       pairs, T, cap, E, expert_offsets, sorted_token, pair_to_sorted, gemm_tile_off);
+    return launch_status();
+  }
   const int n_tiles = perm_tiles(cap);
   int32_t* hist = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(perm_hist_kernel, dim3(n_tiles), dim3(PM_THREADS), 0, s, pair_expert, pairs,
