@@ -17,17 +17,17 @@ constexpr int kGemmBM = 128;   // M tile (rows) of the grouped SwiGLU GEMM
 // ---- bf16 <-> fp32 ------------------------------------------------------------------
 RFX_DEVICE float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
-// Round to nearest, ties to even.  Inputs here are finite; NaN maps to a quiet NaN.
-RFX_DEVICE uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
+// Round to nearest, ties to even, with the hardware conversion (v_cvt_pk_bf16_f32).
+// Inputs here are finite.
+typedef float rfx_f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 rfx_bf16x2 __attribute__((ext_vector_type(2)));
 
 RFX_DEVICE uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  const rfx_f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, rfx_bf16x2));
 }
+
+RFX_DEVICE uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
 
 // ---- wave64 reductions ----------------------------------------------------------------
 RFX_DEVICE int wave_sum_i32(int v) {

@@ -349,9 +349,10 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
             const int c = wn * (GM_BROWS / 4) + 32 * j + 8 * g + ccol;
             float a4[4];
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
+            for (int h = 0; h < 4; ++h) {     // SiLU(g) u = g u / (1 + e^-g), e^x = 2^(x log2 e)
               const float gg = acc[i][j][4 * g + h], uu = acc[i][j + GM_NT / 2][4 * g + h];
-              a4[h] = gg / (1.0f + expf(-gg)) * uu;
+              const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
+              a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
             }
             if (t.n0 + c < N_out)
               *reinterpret_cast<uint2*>(orow + c) =
