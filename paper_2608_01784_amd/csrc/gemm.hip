@@ -61,7 +61,13 @@ constexpr int GM_UP_BN = GM_BROWS / 2;     // activation columns per up-GEMM til
 constexpr int GM_DOWN_BN = GM_BROWS;       // output columns per down-GEMM tile
 constexpr int GM_B_ELEMS = GM_BROWS * GM_BK;   // B slice
 constexpr int GM_XCDS = 8;
-constexpr int GM_NT = GM_BROWS / 64;       // 32-wide B sub-tiles per compute wave
+#ifndef RFX_GEMM_CW
+#define RFX_GEMM_CW 4
+#endif
+constexpr int GM_CW = RFX_GEMM_CW;         // compute waves: 2 (M) x GM_WN (N)
+constexpr int GM_WN = GM_CW / 2;
+constexpr int GM_NT = GM_BROWS / (32 * GM_WN);   // 32-wide B sub-tiles per compute wave
+static_assert(GM_CW == 4 || GM_CW == 8, "compute waves");
 // LDS rows are BK bf16 = CH chunks of 16 bytes; one DMA op (a wave, 64 lanes x 16
 // bytes = 1 KB) fills ROWS_PER_OP whole rows.  Chunk c of row r sits in slot
 // c ^ ((r / RG) % CH), RG = 16 / CH: the 16 rows one 16-lane group reads cover all
@@ -70,7 +76,7 @@ constexpr int GM_CH = GM_BK / 8;
 constexpr int GM_ROWS_PER_OP = 64 / GM_CH;
 constexpr int GM_RG = 16 / GM_CH;
 constexpr int GM_BM = kGemmBM;
-constexpr int GM_THREADS = 512;            // 4 compute + 4 loading waves
+constexpr int GM_THREADS = 64 * (GM_CW + 4);   // compute waves + 4 loading waves
 constexpr int GM_STAGES = RFX_GEMM_STAGES;
 constexpr int GM_A_ELEMS = GM_BM * GM_BK;
 constexpr int GM_STAGE_ELEMS = GM_A_ELEMS + GM_B_ELEMS;
@@ -90,16 +96,16 @@ struct Tile {
 // LDS copies; the expert is found in one round: every lane tests up to 4 experts
 // and the wave counts those whose first tile lies at or before L (tile_off is
 // nondecreasing, so that count minus one is the expert).  L is wave-uniform.
-template <int BN>
+template <int BM, int BN>
 __device__ __forceinline__ Tile decode_tile(int L, const int32_t* tile_off,
                                             const int32_t* expert_offsets, int E, int dense_M,
                                             int n_tiles, int out_rows) {
   Tile t;
   if (dense_M >= 0) {
-    const int mt = (dense_M + GM_BM - 1) / GM_BM;
+    const int mt = (dense_M + BM - 1) / BM;
     t.expert = 0;
     t.n0 = (L / mt) * BN;
-    t.row0 = (L % mt) * GM_BM;
+    t.row0 = (L % mt) * BM;
     t.row_end = dense_M;
     return t;
   }
@@ -116,11 +122,11 @@ __device__ __forceinline__ Tile decode_tile(int L, const int32_t* tile_off,
   t.expert = lo;
 #if RFX_GEMM_NINNER
   t.n0 = (local % n_tiles) * BN;
-  t.row0 = expert_offsets[lo] + (local / n_tiles) * GM_BM;
+  t.row0 = expert_offsets[lo] + (local / n_tiles) * BM;
 #else
   const int mt = tile_off[lo + 1] - tile_off[lo];
   t.n0 = (local / mt) * BN;
-  t.row0 = expert_offsets[lo] + (local % mt) * GM_BM;
+  t.row0 = expert_offsets[lo] + (local % mt) * BM;
 #endif
   const int re = expert_offsets[lo + 1];
   t.row_end = re < out_rows ? re : out_rows;
@@ -136,16 +142,18 @@ __device__ __forceinline__ void waitcnt_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
 }
 
-// Each step issues GM_OPS vector-memory ops per loading wave; let the ops of
-// `pending` later steps stay outstanding.
-__device__ __forceinline__ void wait_vm(int pending) {
-  static_assert(GM_STAGES >= 2 && GM_STAGES <= 6, "stage count");
+// Each step issues OPS vector-memory ops per loading wave; let the ops of `pending`
+// later steps stay outstanding.  Ops complete in issue order, so anything issued
+// after them (epilogue stores) only makes the wait longer, never too short.
+template <int OPS, int STAGES>
+__device__ __forceinline__ void wait_steps(int pending) {
+  static_assert(STAGES >= 2 && STAGES <= 6, "stage count");
   switch (pending) {
     case 0: waitcnt_vm<0>(); break;
-    case 1: waitcnt_vm<GM_OPS>(); break;
-    case 2: waitcnt_vm<(GM_STAGES > 3 ? 2 * GM_OPS : 0)>(); break;
-    case 3: waitcnt_vm<(GM_STAGES > 4 ? 3 * GM_OPS : 0)>(); break;
-    default: waitcnt_vm<(GM_STAGES > 5 ? 4 * GM_OPS : 0)>(); break;
+    case 1: waitcnt_vm<(STAGES > 2 ? OPS : 0)>(); break;
+    case 2: waitcnt_vm<(STAGES > 3 ? 2 * OPS : 0)>(); break;
+    case 3: waitcnt_vm<(STAGES > 4 ? 3 * OPS : 0)>(); break;
+    default: waitcnt_vm<(STAGES > 5 ? 4 * OPS : 0)>(); break;
   }
 }
 
@@ -164,6 +172,57 @@ __device__ __forceinline__ void lds_dma(const uint16_t* src, uint16_t* dst) {
 // the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Epilogue of one compute wave: its 64 x (32 NT) accumulator block (2 x NT MFMA
+// tiles, weights as the A operand) to bf16 rows of `out`.  Lane l, register r holds
+// output row l % 32 (a pair row) and column 8 (r/4) + 4 (l/32) + r%4 of its 32 x 32
+// block, so registers 4g..4g+3 are 4 consecutive columns: one 8-byte store each.
+// UP: sub-tiles j and j + NT/2 hold gate and up of the same columns and the store
+// is SiLU(g) u.  Rows at or past the tile's row_end are skipped; N is a multiple of
+// 64, so a group of 4 columns is wholly inside a partial last N tile or wholly past it.
+template <bool UP, int NT>
+__device__ __forceinline__ void store_wave_tile(const f32x16_t (&acc)[2][NT], const Tile& t,
+                                                int row_in_tile, int col0, int N_out,
+                                                uint16_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63, ccol = 4 * (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int grow = t.row0 + row_in_tile + 32 * i + (lane & 31);
+    if (grow >= t.row_end) continue;
+    uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
+    if (UP) {
+#pragma unroll
+      for (int j = 0; j < NT / 2; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int c = col0 + 32 * j + 8 * g + ccol;
+          float a4[4];
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {     // SiLU(g) u = g u / (1 + e^-g), e^x = 2^(x log2 e)
+            const float gg = acc[i][j][4 * g + h], uu = acc[i][j + NT / 2][4 * g + h];
+            const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
+            a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
+          }
+          if (t.n0 + c < N_out)
+            *reinterpret_cast<uint2*>(orow + c) =
+                make_uint2(pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3]));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int c = col0 + 32 * j + 8 * g + ccol;
+          const f32x16_t& a = acc[i][j];
+          if (t.n0 + c < N_out)
+            *reinterpret_cast<uint2*>(orow + c) =
+                make_uint2(pack_bf16x2(a[4 * g], a[4 * g + 1]), pack_bf16x2(a[4 * g + 2], a[4 * g + 3]));
+        }
+      }
+    }
+  }
 }
 
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
@@ -206,9 +265,9 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool producer = wave >= 4;
-  const int wv = wave & 3;          // index among the loading (and among the computing) waves
-  const int wm = wv >> 1, wn = wv & 1;
+  const bool producer = wave >= GM_CW;
+  const int wv = producer ? wave - GM_CW : wave;   // index among the loading / computing waves
+  const int wm = wv / GM_WN, wn = wv % GM_WN;
 
   if (producer) {
     // ---- loading waves: run GM_STAGES-1 steps ahead of the multiply ----
@@ -223,7 +282,7 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     const uint16_t* b_ptr[GM_B_OPS];
     int ld_tile = -1;
     auto setup_loader = [&](int tile_i) {
-      const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
+      const Tile t = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
                                      n_tiles, out_rows);
       const int rows_valid = t.row_end - t.row0;
 #pragma unroll
@@ -277,7 +336,7 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     };
     for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
     for (int s = 0; s < n_steps; ++s) {
-      wait_vm(min(GM_STAGES - 2, n_steps - 1 - s));
+      wait_steps<GM_OPS, GM_STAGES>(min(GM_STAGES - 2, n_steps - 1 - s));
       lds_barrier();       // slice s visible to all waves; slice s-1 no longer read
       if (s + GM_STAGES - 1 < n_steps) issue(s + GM_STAGES - 1);
     }
@@ -291,9 +350,9 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
   int b_row[GM_NT];
 #pragma unroll
   for (int j = 0; j < GM_NT; ++j)
-    b_row[j] = UP ? (j < GM_NT / 2 ? wn * (GM_BROWS / 4) + 32 * j
-                                   : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - GM_NT / 2))
-                  : wn * (GM_BROWS / 2) + 32 * j;
+    b_row[j] = UP ? (j < GM_NT / 2 ? wn * (GM_BROWS / 2 / GM_WN) + 32 * j
+                                   : GM_BROWS / 2 + wn * (GM_BROWS / 2 / GM_WN) + 32 * (j - GM_NT / 2))
+                  : wn * (GM_BROWS / GM_WN) + 32 * j;
   const int a_row[2] = {wm * 64, wm * 64 + 32};
   // fragment rows are 32-aligned bases + (lane % 32): (row / RG) % CH from lane % 32
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / GM_RG) % GM_CH;
@@ -310,69 +369,250 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
       lds_barrier();       // slice s visible to all waves; slice s-1 no longer read
       const uint16_t* As = smem + (s % GM_STAGES) * GM_STAGE_ELEMS;
       const uint16_t* Bs = As + GM_A_ELEMS;
-#pragma unroll
-      for (int kk = 0; kk < GM_BK / 16; ++kk) {
+      // 16-wide K sub-steps; the fragments of sub-step kk+1 are read from LDS into
+      // the other register set before the MFMAs of kk are issued, so the LDS latency
+      // hides behind them (only the first read after the barrier is exposed)
+      bf16x8_t af[2][2], bfr[2][GM_NT];
+      auto load = [&](int kk, int buf) {
         const int slot = ((2 * kk + fsel) ^ fx) * 8;
-        bf16x8_t af[2], bfr[GM_NT];
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-          af[i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
+          af[buf][i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * GM_BK + slot);
 #pragma unroll
         for (int j = 0; j < GM_NT; ++j)
-          bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
+          bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
+      };
+      // (the instruction scheduler is told the order: reads of kk+1, then MFMAs of kk)
+      constexpr int kReads = 2 + GM_NT, kMfmas = 2 * GM_NT;
+      load(0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);      // LDS reads
+#pragma unroll
+      for (int kk = 0; kk < GM_BK / 16; ++kk) {
+        if (kk + 1 < GM_BK / 16) {
+          load(kk + 1, (kk + 1) & 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+        }
         // weights as the MFMA's A operand: the accumulator is the transposed tile,
         // so each lane ends up holding 4 consecutive output columns of one row
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < GM_NT; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
+                                                                acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);    // MFMAs
       }
     }
-    // epilogue: lane l, register r holds output row l % 32 (a pair row) and column
-    // 8 (r/4) + 4 (l/32) + r%4 of its 32 x 32 block, so registers 4g..4g+3 are 4
-    // consecutive columns: one 8-byte store each.  N is a multiple of 64, so a
-    // group of 4 is either wholly inside a partial last N tile or wholly past it.
-    const Tile t = decode_tile<BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
-                                   n_tiles, out_rows);
-    const int ccol = 4 * (lane >> 5);
+    const Tile t = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
+                                          n_tiles, out_rows);
+    store_wave_tile<UP, GM_NT>(acc, t, wm * 64,
+                               UP ? wn * (GM_BROWS / 2 / GM_WN) : wn * (GM_BROWS / GM_WN), N_out, out);
+  }
+}
+
+// ---- tall tiles: 256 rows x 256 weight rows, 8 waves that all load and multiply ----
+//
+// For experts with many rows the MFMAs, not the weight stream, are the bound.  Two
+// waves share each SIMD, each multiplying a 64 x 128 block (4 x 2 waves over the
+// 256 x 256 tile), so one wave's LDS reads, barrier waits and epilogue overlap the
+// other's MFMAs; every wave issues its share of the global->LDS copies right after
+// the step barrier, into the slice the previous step has just released.  The M tile
+// is 256 rows, so per expert the tiles are ceil(n_e / 256), counted in LDS at start.
+#ifndef RFX_TALL_BK
+#define RFX_TALL_BK 64
+#endif
+#ifndef RFX_TALL_STAGES
+#define RFX_TALL_STAGES 2
+#endif
+#ifndef RFX_TALL_MIN_ROWS
+#define RFX_TALL_MIN_ROWS 512
+#endif
+constexpr int TL_BM = 2 * kGemmBM;
+constexpr int TL_BK = RFX_TALL_BK;
+constexpr int TL_STAGES = RFX_TALL_STAGES;
+constexpr int TL_WAVES = 8;
+constexpr int TL_THREADS = 64 * TL_WAVES;
+constexpr int TL_NT = 4;                         // 32-row B sub-tiles per wave
+constexpr int TL_CH = TL_BK / 8;
+constexpr int TL_ROWS_PER_OP = 64 / TL_CH;
+constexpr int TL_RG = 16 / TL_CH;
+constexpr int TL_A_ELEMS = TL_BM * TL_BK;
+constexpr int TL_B_ELEMS = GM_BROWS * TL_BK;
+constexpr int TL_STAGE_ELEMS = TL_A_ELEMS + TL_B_ELEMS;
+constexpr int TL_A_OPS = TL_BM / TL_ROWS_PER_OP / TL_WAVES;   // DMA ops per wave per step
+constexpr int TL_B_OPS = GM_BROWS / TL_ROWS_PER_OP / TL_WAVES;
+constexpr int TL_OPS = TL_A_OPS + TL_B_OPS;
+constexpr size_t TL_LDS = size_t(TL_STAGES) * TL_STAGE_ELEMS * sizeof(uint16_t);
+static_assert(TL_BK == 32 || TL_BK == 64, "tall BK");
+static_assert(GM_BROWS == 256, "tall tiles: two wave columns of 128 weight rows");
+static_assert(TL_LDS + 8192 <= 160 * 1024, "tall LDS ring");
+
+template <bool UP>
+__global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
+    const uint16_t* __restrict__ x, const int32_t* __restrict__ gather,
+    const int32_t* __restrict__ expert_offsets, int E, const uint16_t* __restrict__ w0,
+    const uint16_t* __restrict__ w1, size_t w_expert_stride, int K, int N_out, int x_rows,
+    int out_rows, int packed, uint16_t* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
+  const int n_tiles = (N_out + BN - 1) / BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // expert row offsets and the per-expert prefix of 256-row tiles
+  __shared__ int s_tile_off[REFLEX_MAX_EXPERTS + 1], s_eo[REFLEX_MAX_EXPERTS + 1];
+  __shared__ int s_part[TL_WAVES];
+  for (int e = tid; e <= E; e += TL_THREADS) s_eo[e] = expert_offsets[e];
+  __syncthreads();
+  {
+    int n = 0;
+    if (tid < E) {
+      n = s_eo[tid + 1] - s_eo[tid];
+      n = n < 0 ? 0 : (n + TL_BM - 1) / TL_BM;
+    }
+    const int incl = wave_inclusive_scan_i32(n, lane);
+    if (lane == 63) s_part[wave] = incl;
+    __syncthreads();
+    int base = incl - n;
+    for (int q = 0; q < wave; ++q) base += s_part[q];
+    if (tid <= E) s_tile_off[tid] = base;       // tid == E: the total
+    __syncthreads();
+  }
+  const int total = s_tile_off[E] * n_tiles;
+  const int xcd = blockIdx.x % GM_XCDS;
+  const int per_xcd = gridDim.x / GM_XCDS;
+  const int j0 = blockIdx.x / GM_XCDS;
+  const int chunk = (total + GM_XCDS - 1) / GM_XCDS;
+  const int l_begin = xcd * chunk + j0;
+  const int l_end = min(total, (xcd + 1) * chunk);
+  if (l_begin >= l_end) return;
+  const int n_my = (l_end - l_begin + per_xcd - 1) / per_xcd;
+  const int nk = K / TL_BK;
+  const int n_steps = n_my * nk;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // ---- copies: op q of the step fills rows ROWS_PER_OP q ..; lane L writes row
+  // r = ROWS_PER_OP q + L / CH at slot L % CH, holding chunk (L % CH) ^ ((r / RG) % CH)
+  auto lane_row = [&](int q) { return q * TL_ROWS_PER_OP + lane / TL_CH; };
+  auto lane_chunk = [&](int q) { return ((lane % TL_CH) ^ ((lane_row(q) / TL_RG) % TL_CH)) * 8; };
+  const uint16_t* a_ptr[TL_A_OPS];
+  const uint16_t* b_ptr[TL_B_OPS];
+  int ld_tile = -1;
+  auto setup_loader = [&](int tile_i) {
+    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
+                                          n_tiles, out_rows);
+    const int rows_valid = t.row_end - t.row0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int grow = t.row0 + a_row[i] + (lane & 31);
-      if (grow >= t.row_end) continue;
-      uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
-      if (UP) {
+    for (int j = 0; j < TL_A_OPS; ++j) {
+      const int r = lane_row(TL_A_OPS * wave + j);
+      int src = t.row0 + (r < rows_valid ? r : 0);     // rows past the expert reuse row0
+      if (rows_valid <= 0) src = 0;
+      if (UP && gather != nullptr) {
+        src = gather[src];
+        src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
+      }
+      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(TL_A_OPS * wave + j);
+    }
+    if (packed) {     // packed slices are the LDS images of 64-wide K steps (TL_BK == GM_BK)
+      const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
 #pragma unroll
-        for (int j = 0; j < GM_NT / 2; ++j) {
+      for (int j = 0; j < TL_B_OPS; ++j)
+        b_ptr[j] = w0 + slice0 * TL_B_ELEMS + (TL_B_OPS * wave + j) * 512 + lane * 8;
+    } else {
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int c = wn * (GM_BROWS / 4) + 32 * j + 8 * g + ccol;
-            float a4[4];
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {     // SiLU(g) u = g u / (1 + e^-g), e^x = 2^(x log2 e)
-              const float gg = acc[i][j][4 * g + h], uu = acc[i][j + GM_NT / 2][4 * g + h];
-              const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
-              a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
-            }
-            if (t.n0 + c < N_out)
-              *reinterpret_cast<uint2*>(orow + c) =
-                  make_uint2(pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3]));
-          }
+      for (int j = 0; j < TL_B_OPS; ++j) {
+        const int r = lane_row(TL_B_OPS * wave + j);
+        const uint16_t* wb;
+        int wr;
+        if (UP) {
+          wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
+          wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
+        } else {
+          wb = w0 + t.expert * w_expert_stride;
+          wr = t.n0 + r;
         }
-      } else {
-#pragma unroll
-        for (int j = 0; j < GM_NT; ++j) {
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int c = wn * (GM_BROWS / 2) + 32 * j + 8 * g + ccol;
-            const f32x16_t& a = acc[i][j];
-            if (t.n0 + c < N_out)
-              *reinterpret_cast<uint2*>(orow + c) =
-                  make_uint2(pack_bf16x2(a[4 * g], a[4 * g + 1]), pack_bf16x2(a[4 * g + 2], a[4 * g + 3]));
-          }
-        }
+        wr = wr < N_out ? wr : N_out - 1;
+        b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(TL_B_OPS * wave + j);
       }
     }
+  };
+  auto issue = [&](int step) {
+    const int tile_i = step / nk, kt = step - tile_i * nk;
+    if (tile_i != ld_tile) {
+      setup_loader(tile_i);
+      ld_tile = tile_i;
+    }
+    uint16_t* As = smem + (step % TL_STAGES) * TL_STAGE_ELEMS;
+    uint16_t* Bs = As + TL_A_ELEMS;
+    const int k0 = kt * TL_BK;
+    const size_t kb = packed ? static_cast<size_t>(kt) * TL_B_ELEMS : static_cast<size_t>(k0);
+#pragma unroll
+    for (int j = 0; j < TL_A_OPS; ++j)
+      lds_dma(a_ptr[j] + k0, As + (TL_A_OPS * wave + j) * 512);
+#pragma unroll
+    for (int j = 0; j < TL_B_OPS; ++j) lds_dma(b_ptr[j] + kb, Bs + (TL_B_OPS * wave + j) * 512);
+  };
+
+  // ---- multiply: B sub-tiles as in the 128-row kernel with two wave columns ----
+  int b_row[TL_NT];
+#pragma unroll
+  for (int j = 0; j < TL_NT; ++j)
+    b_row[j] = UP ? (j < TL_NT / 2 ? wn * (GM_BROWS / 4) + 32 * j
+                                   : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - TL_NT / 2))
+                  : wn * (GM_BROWS / 2) + 32 * j;
+  const int a_row[2] = {wm * 64, wm * 64 + 32};
+  const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
+  f32x16_t acc[2][TL_NT];
+
+  for (int s0 = 0; s0 < TL_STAGES - 1 && s0 < n_steps; ++s0) issue(s0);
+  int s = 0;
+  for (int tile_i = 0; tile_i < n_my; ++tile_i) {
+    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
+                                          n_tiles, out_rows);
+    const bool active = t.row0 + wm * 64 < t.row_end;     // this wave's rows hold pairs
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < TL_NT; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int kt = 0; kt < nk; ++kt, ++s) {
+      wait_steps<TL_OPS, TL_STAGES>(min(TL_STAGES - 2, n_steps - 1 - s));
+      lds_barrier();       // slice s complete and visible; slice s-1 no longer read
+      if (s + TL_STAGES - 1 < n_steps) issue(s + TL_STAGES - 1);
+      if (!active) continue;
+      const uint16_t* As = smem + (s % TL_STAGES) * TL_STAGE_ELEMS;
+      const uint16_t* Bs = As + TL_A_ELEMS;
+      bf16x8_t af[2][2], bfr[2][TL_NT];
+      auto load = [&](int kk, int buf) {
+        const int slot = ((2 * kk + fsel) ^ fx) * 8;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          af[buf][i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * TL_BK + slot);
+#pragma unroll
+        for (int j = 0; j < TL_NT; ++j)
+          bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * TL_BK + slot);
+      };
+      constexpr int kReads = 2 + TL_NT, kMfmas = 2 * TL_NT;
+      load(0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+#pragma unroll
+      for (int kk = 0; kk < TL_BK / 16; ++kk) {
+        if (kk + 1 < TL_BK / 16) {
+          load(kk + 1, (kk + 1) & 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < TL_NT; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
+                                                                acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);
+      }
+    }
+    if (active)
+      store_wave_tile<UP, TL_NT>(acc, t, wm * 64, UP ? wn * (GM_BROWS / 4) : wn * (GM_BROWS / 2),
+                                 N_out, out);
   }
 }
 
@@ -472,6 +712,30 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
   return launch_status();
 }
 
+// Tall tiles where an expert would average RFX_TALL_MIN_ROWS rows or more at full
+// pair capacity (the MFMAs, not the weight stream, bound such launches).
+bool use_tall(int cap, int E, bool packed) {
+  return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS &&
+         (!packed || TL_BK == GM_BK);
+}
+
+template <bool UP>
+int launch_gemm_tall(const uint16_t* x, const int32_t* gather, const int32_t* eo, int E,
+                     const uint16_t* w0, const uint16_t* w1, size_t stride, int K, int N, int x_rows,
+                     int out_rows, int packed, uint16_t* out, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&swiglu_gemm_tall_kernel<UP>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(TL_LDS)) != hipSuccess)
+      return REFLEX_ERR_LAUNCH;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(swiglu_gemm_tall_kernel<UP>, dim3(persistent_grid()), dim3(TL_THREADS), TL_LDS,
+                     s, x, gather, eo, E, w0, w1, stride, K, N, x_rows, out_rows, packed, out);
+  return launch_status();
+}
+
 }  // namespace
 
 size_t swiglu_ws_bytes(int pair_capacity, int E, int f) {
@@ -497,6 +761,10 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
                      const uint16_t* wg, const uint16_t* wu, const uint16_t* w_packed, int T, int E,
                      int d, int f, int cap, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
+  if (use_tall(cap, E, w_packed != nullptr))
+    return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, w_packed ? w_packed : wg, wu,
+                                  static_cast<size_t>(f) * d, d, f, T, cap, w_packed != nullptr,
+                                  routed_act(ws, E), s);
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
                            w_packed ? w_packed : wg, wu, static_cast<size_t>(f) * d, d, f, T, cap,
                            w_packed != nullptr, routed_act(ws, E), s);
@@ -505,6 +773,10 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
 int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, const uint16_t* w_packed,
                        int E, int d, int f, int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
+  if (use_tall(cap, E, w_packed != nullptr))
+    return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E,
+                                   w_packed ? w_packed : wd, nullptr, static_cast<size_t>(d) * f, f,
+                                   d, cap, cap, w_packed != nullptr, y_sorted, s);
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
                             expert_offsets, E, -1, w_packed ? w_packed : wd, nullptr,
                             static_cast<size_t>(d) * f, f, d, cap, cap, w_packed != nullptr,
