@@ -36,7 +36,10 @@ DEFAULT_WORKLOAD = "lladamoe_t1024_e64"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 COPY_CAL_BYTES = 1 << 28       # the plain device copy that calibrates the byte counters
 # rocprofv3 kernel names of the stages with a counter-derived traffic figure
-STAGE_KERNELS = {"gemm_up": "swiglu_gemm_kernel<true>", "gemm_down": "swiglu_gemm_kernel<false>"}
+# the grouped GEMM's kernels per stage: 128-row tiles, or 256-row tiles for launches
+# whose experts average many rows (the library picks one per launch)
+STAGE_KERNELS = {"gemm_up": ("swiglu_gemm_kernel<true>", "swiglu_gemm_tall_kernel<true>"),
+                 "gemm_down": ("swiglu_gemm_kernel<false>", "swiglu_gemm_tall_kernel<false>")}
 
 
 def log(msg):
@@ -151,34 +154,41 @@ def kernel_source_digest() -> str:
 
 
 def _counter_rows(path):
-    """(kernel name, counter, value) of every dispatch in a rocprofv3 counter CSV."""
+    """(kernel name, counter, value) of every dispatch in a rocprofv3 counter CSV, in
+    dispatch order."""
     rows = []
     with open(path, newline="") as fh:
         for r in csv.DictReader(fh):
             name = r["Kernel_Name"].replace("void ", "").replace("rfx::(anonymous namespace)::", "")
             name = re.sub(r"\(.*", "", name)
-            rows.append((name, r["Counter_Name"], float(r["Counter_Value"])))
-    return rows
+            rows.append((int(r.get("Dispatch_Id") or len(rows)), name, r["Counter_Name"],
+                         float(r["Counter_Value"])))
+    rows.sort(key=lambda t: t[0])
+    return [t[1:] for t in rows]
 
 
-def _per_dispatch_kib(path, counter, kernel=None):
-    """Mean counter value (KiB) per dispatch of `kernel`; without a kernel name, of the
-    dispatches with the largest reading (the calibration copy)."""
+def _per_dispatch_kib(path, counter, kernel=None, stride=1):
+    """Mean counter value (KiB) per dispatch of `kernel` (every `stride`-th of its
+    dispatches from the first); without a kernel name, of the dispatches with the largest
+    reading (the calibration copy)."""
     vals = [(n, v) for n, c, v in _counter_rows(path) if c == counter]
     if kernel is None:
         top = max(v for _, v in vals)
         sel = [v for _, v in vals if v >= 0.5 * top]
     else:
-        sel = [v for n, v in vals if n == kernel]
+        sel = [v for n, v in vals if n == kernel][::stride]
     if not sel:
         raise SystemExit(f"no {counter} dispatches of {kernel or 'the copy'} in {path}")
     return sum(sel) / len(sel), len(sel)
 
 
-def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
+               shared=False):
     """Turn two rocprofv3 --pmc runs of the bench (FETCH_SIZE, WRITE_SIZE) and the same two
     counters on a plain copy of COPY_CAL_BYTES into HBM bytes per GEMM launch, stored in
-    the traffic file under the current GEMM source digest."""
+    the traffic file under the current GEMM source digest.  With a shared expert
+    (`shared`), every forward launches each GEMM kernel twice, routed experts first and
+    the shared expert's dense GEMM after; only the routed launches are counted."""
     cf, _ = _per_dispatch_kib(copy_fetch_csv, "FETCH_SIZE")
     cw, _ = _per_dispatch_kib(copy_write_csv, "WRITE_SIZE")
     k_fetch = COPY_CAL_BYTES / (cf * 1024.0)      # true read bytes per counted byte
@@ -191,9 +201,12 @@ def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_writ
                            "write_kib": round(cw, 1), "fetch_factor": round(k_fetch, 4),
                            "write_factor": round(k_write, 4)}
     digest = kernel_source_digest()
-    for stage, kname in STAGE_KERNELS.items():
-        fk, nf = _per_dispatch_kib(fetch_csv, "FETCH_SIZE", kname)
-        wk, nw = _per_dispatch_kib(write_csv, "WRITE_SIZE", kname)
+    for stage, knames in STAGE_KERNELS.items():
+        present = {n for n, c, _ in _counter_rows(fetch_csv) if c == "FETCH_SIZE"}
+        kname = next((k for k in knames if k in present), knames[0])
+        stride = 2 if shared and kname in STAGE_KERNELS[stage][:1] else 1
+        fk, nf = _per_dispatch_kib(fetch_csv, "FETCH_SIZE", kname, stride)
+        wk, nw = _per_dispatch_kib(write_csv, "WRITE_SIZE", kname, stride)
         ent = {"workload": workload, "expert_weights": layout, "kernel": stage,
                "kernel_name": kname, "source_sha256": digest,
                "fetch_kib_per_dispatch": round(fk, 1), "write_kib_per_dispatch": round(wk, 1),
@@ -389,7 +402,9 @@ def main():
     a = ap.parse_args()
     layout = "packed at load" if a.packed_weights else "row-major"
     if a.ingest_pmc:
-        ingest_pmc(a.workload, layout, *a.ingest_pmc)
+        from synth import make_workload
+        ingest_pmc(a.workload, layout, *a.ingest_pmc,
+                   shared=make_workload(a.workload, seed=a.seed).f_shared > 0)
         return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
