@@ -38,6 +38,7 @@ COPY_CAL_BYTES = 1 << 28       # the plain device copy that calibrates the byte 
 # rocprofv3 kernel names of the stages with a counter-derived traffic figure
 # the grouped GEMM's kernels per stage: 128-row tiles, or 256-row tiles for launches
 # whose experts average many rows (the library picks one per launch)
+MALL_FLUSH_BYTES = 512 << 20   # read before each cold step: twice the Infinity Cache
 STAGE_KERNELS = {"gemm_up": ("swiglu_gemm_kernel<true>", "swiglu_gemm_tall_kernel<true>"),
                  "gemm_down": ("swiglu_gemm_kernel<false>", "swiglu_gemm_tall_kernel<false>")}
 
@@ -248,12 +249,24 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_CAL_BYTES, "copies": 3}))
 
 
-def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: HipEvents):
+def _dist(xs):
+    """Median and 10th / 90th percentiles of per-step times (ms)."""
+    import numpy as np
+    v = np.asarray(xs, dtype=np.float64)
+    return {"median": round(float(np.median(v)), 4), "p10": round(float(np.percentile(v, 10)), 4),
+            "p90": round(float(np.percentile(v, 90)), 4)}
+
+
+def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: HipEvents,
+             cold=False):
     """Time `steps` steps of the layer (or layer stack) through the plain fused entry
-    point (wall clock and one event pair around all of them), then run `steps` more
-    through the timed entry point for the per-stage split (its events add a little
-    time of their own, so that pass is kept out of the step time).  Returns timings and
-    the layer objects used."""
+    point (wall clock and one event pair around all of them), then `steps` more with an
+    event pair around each (the per-step distribution), then `steps` more through the
+    timed entry point for the per-stage split (its events add a little time of their
+    own, so those passes are kept out of the step time).  With `cold`, a last pass of
+    `steps` timed-entry steps reads a MALL_FLUSH_BYTES buffer before each step, so the
+    256 MB Infinity Cache holds none of the weights when a step starts.  Returns timings
+    and the layer objects used."""
     from paper_2608_01784_amd import _lib
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer
     L = w.n_layers
@@ -292,15 +305,41 @@ def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: 
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     gpu_step_ms = ev.ms(e_begin, e_end) / steps
+    marks = [ev.create() for _ in range(steps + 1)]
+    ev.record(marks[0])
     for s in range(steps):
-        step(evs[s])
+        step()
+        ev.record(marks[s + 1])
     torch.cuda.synchronize()
-    stage_ms = {}
-    for i, name in enumerate(_lib.STAGES):
-        stage_ms[name] = sum(ev.ms(evs[s][l][i], evs[s][l][i + 1]) for s in range(steps)
-                             for l in range(L)) / (steps * L)
-    return {"wall_ms": (t1 - t0) * 1e3 / steps, "gpu_ms": gpu_step_ms, "stage_ms": stage_ms,
-            "layers": lays}
+    per_step = [ev.ms(marks[s], marks[s + 1]) for s in range(steps)]
+
+    def stage_pass(flush):
+        for s in range(steps):
+            if flush is not None:
+                # read (not write) the buffer: the cache ends up holding only clean lines
+                # of it, so no write-back of dirty lines competes with the step
+                flush.max()
+            step(evs[s])
+        torch.cuda.synchronize()
+        n_ev = _lib.N_STAGE_EVENTS
+        stage = {}
+        for i, name in enumerate(_lib.STAGES):
+            stage[name] = sum(ev.ms(evs[s][l][i], evs[s][l][i + 1]) for s in range(steps)
+                              for l in range(L)) / (steps * L)
+        totals = [sum(ev.ms(evs[s][l][0], evs[s][l][n_ev - 1]) for l in range(L))
+                  for s in range(steps)]
+        return stage, totals
+
+    stage_ms, _ = stage_pass(None)
+    out = {"wall_ms": (t1 - t0) * 1e3 / steps, "gpu_ms": gpu_step_ms, "stage_ms": stage_ms,
+           "step_dist": _dist(per_step), "layers": lays}
+    if cold:
+        flush = torch.ones(MALL_FLUSH_BYTES // 4, dtype=torch.int32, device=h0.device)
+        c_stage, c_tot = stage_pass(flush)
+        del flush
+        out["cold"] = {"stage_ms": c_stage, "step_dist": _dist(c_tot),
+                       "flush_bytes": MALL_FLUSH_BYTES}
+    return out
 
 
 def cpu_baseline(w, host, seconds):
@@ -389,6 +428,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-uniform", action="store_true")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the pass that evicts the Infinity Cache (a 512 MiB read) before "
+                         "each step")
     ap.add_argument("--packed-weights", action="store_true",
                     help="pack the expert weights once (reflex_pack_*) and stream the packed layout")
     ap.add_argument("--trajectory", action="store_true",
@@ -457,7 +499,8 @@ def main():
 
     ev = HipEvents()
     log(f"timing variable-K path: {a.warmup} warmup + {a.steps} steps")
-    var = run_path(torch, w, dws, residuals, h0, state, 0, a.steps, a.warmup, ev)
+    var = run_path(torch, w, dws, residuals, h0, state, 0, a.steps, a.warmup, ev,
+                   cold=not a.no_cold)
     lay0 = var["layers"][0]
     P = int(lay0.pairs.item())
     counts = expert_counts(lay0, h0, state, torch)
@@ -495,9 +538,17 @@ def main():
         "pairs_per_layer": P, "avg_k": round(P / T, 4), "experts_touched": touched,
         "max_expert_rows": int(counts.max()), "gpu_ms_per_step": round(var["gpu_ms"], 4),
         "stage_ms": {k: round(v, 5) for k, v in stages.items()},
+        "step_ms_dist": var["step_dist"],
         "roofline": roof,
         "roofline_all": roof_all,
     }
+    if "cold" in var:
+        cs = var["cold"]["stage_ms"]
+        out["cold"] = {"flush_bytes": var["cold"]["flush_bytes"],
+                       "step_ms_dist": var["cold"]["step_dist"],
+                       "stage_ms": {k: round(v, 5) for k, v in cs.items()},
+                       "roofline": {s: stage_roofline(s, cs[s], d, f, P, touched, T, E)
+                                    for s in ("gemm_up", "gemm_down")}}
     if uni is not None:
         lu = uni["layers"][0]
         Pu = int(lu.pairs.item())
