@@ -85,6 +85,28 @@ def test_router_logits(torch, name):
     assert err.max() <= 1e-4
 
 
+@pytest.mark.parametrize("T,d,E,with_bias", [(4100, 384, 100, True), (4096, 128, 8, False),
+                                             (9000, 128, 37, False), (16400, 128, 250, False),
+                                             (20000, 256, 200, True)])
+def test_router_logits_large_t(torch, T, d, E, with_bias):
+    # T >= 4096: the register kernel with 64 x 64 tiles, and where 128 x 64 tiles number
+    # 512 or more (the last two cases) the LDS-staged kernel; ragged last token tile and
+    # expert counts that are not a multiple of the 64-expert tile
+    w = make_fuzz_workload(300 + T % 97, T=T, d=d, E=E, f=64)
+    rng = np.random.default_rng([T, d, E])
+    bias = (rng.standard_normal(E) * 0.5).astype(np.float32) if with_bias else None
+    wr = w.w_router()
+    logits = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    _lib().reflex_router_logits(to_device(w.h), to_device(wr),
+                                None if bias is None else to_device(bias), logits)
+    torch.cuda.synchronize()
+    got = logits.cpu().numpy().astype(np.float64)
+    ref = oracle.router_scores(w.h, wr, bias)
+    err = np.abs(got - ref) / np.maximum(np.abs(ref).max(axis=1, keepdims=True), 1e-30)
+    note(f"router T={T} d={d} E={E}: max row-relative logit error {err.max():.3e}")
+    assert err.max() <= 1e-4
+
+
 # ----------------------------------------------------------------------------- budget
 def gpu_budget(torch, w: Workload, params=None):
     p = w.params if params is None else params
