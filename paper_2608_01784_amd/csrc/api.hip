@@ -75,7 +75,7 @@ int check_rule(int rule, float threshold) {
 }
 
 struct Layout {
-  size_t logits, k, scalar, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
+  size_t logits, k, done, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
       pair_to_sorted, perm, swiglu, y, shared_act, shared_y, total;
 };
 
@@ -93,7 +93,7 @@ bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
   };
   L.logits = take(sizeof(float) * static_cast<size_t>(T) * E);
   L.k = take(sizeof(int32_t) * static_cast<size_t>(T));
-  L.scalar = take(sizeof(int32_t));
+  L.done = take(sizeof(int32_t));
   L.pair_offsets = take(sizeof(int32_t) * (static_cast<size_t>(T) + 1));
   L.pair_expert = take(sizeof(int32_t) * cap);
   L.pair_weight = take(sizeof(float) * cap);
@@ -369,6 +369,8 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   uint16_t* y = static_cast<uint16_t*>(at(L.y));
   void* gws = at(L.swiglu);
 
+  // the fused route kernel's completion counter, zeroed by the router launch
+  int32_t* done = route_fused_sorts(cap) ? static_cast<int32_t*>(at(L.done)) : nullptr;
   RFX_TRY(mark(0));
   const int32_t* k = a->k_in;
   // small layers: scores and counts in one launch (independent work side by side)
@@ -377,10 +379,10 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
     RFX_TRY(launch_front(a->h, a->w_router, a->router_bias, logits, T, d, E, a->block_idx, a->masked,
                          a->hist_len, a->conf_prev1, a->conf_prev2, a->seq_offsets, a->active_block,
-                         a->B, a->params, kb, s));
+                         a->B, a->params, kb, s, done));
     k = kb;
   } else {
-    RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s));
+    RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s, done));
   }
   RFX_TRY(mark(1));
   if (k == nullptr) {
@@ -398,13 +400,16 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     k = kb;
   }
   RFX_TRY(mark(2));
-  // P lives in pair_offsets[T]; the permutation reads it from there
-  RFX_TRY(launch_count_scan(k, T, kcap, pair_offsets, a->pairs_out, s));
-  RFX_TRY(launch_topk(logits, k, T, E, kcap, a->norm_topk, pair_offsets, pair_expert, pair_weight, s));
+  // pair offsets and TopK in one launch (P lives in pair_offsets[T]); short pair lists
+  // are also sorted there, longer ones by the permutation launches.  Either way the
+  // permutation's scan writes the GEMM tile plan at the head of gws.
+  RFX_TRY(launch_route_fused(logits, k, T, E, kcap, a->norm_topk, cap, pair_offsets, pair_expert,
+                             pair_weight, a->pairs_out, done, expert_offsets, sorted_token,
+                             pair_to_sorted, static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(3));
-  // the permutation's scan also writes the GEMM tile plan at the head of gws
-  RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
-                         sorted_token, pair_to_sorted, at(L.perm), static_cast<int32_t*>(gws), s));
+  if (done == nullptr)
+    RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
+                           sorted_token, pair_to_sorted, at(L.perm), static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(4));
   RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up,
                            a->w_gate_up_packed, T, E, d, f, cap, gws, s));

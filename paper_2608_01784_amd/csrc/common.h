@@ -82,8 +82,10 @@ RFX_DEVICE int clamp_count(int k, int k_max) { return k < 0 ? 0 : (k > k_max ? k
 // Each returns REFLEX_OK or REFLEX_ERR_LAUNCH.  Arguments are already validated.
 namespace rfx {
 
+// zero_word (nullable): set to 0 by the launch (the counter the fused route kernel that
+// follows in the same forward expects to find at zero).
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
-                  int d, int E, hipStream_t s);
+                  int d, int E, hipStream_t s, int32_t* zero_word = nullptr);
 
 // pairs_out may be NULL (the fused forward takes P from the count scan instead).
 int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
@@ -99,7 +101,7 @@ int launch_front(const uint16_t* h, const float* w, const float* bias, float* lo
                  int E, const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
                  const float* c1, const float* c2, const int32_t* seq_offsets,
                  const int32_t* active_block, int B, const reflex_alloc_params& p, int32_t* k_out,
-                 hipStream_t s);
+                 hipStream_t s, int32_t* zero_word = nullptr);
 
 // One forward's commitment and state bookkeeping, one workgroup per sequence.
 int launch_advance_state(const float* conf_t, const int32_t* block_idx, const int32_t* seq_offsets,
@@ -117,6 +119,16 @@ int launch_count_rule(const float* logits, int T, int E, int rule, float thresho
 int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
                 hipStream_t s);
+
+// Pair offsets + TopK (+ the permutation when route_fused_sorts(cap), with `done` a
+// device word the preceding launch set to zero; else done must be NULL and
+// launch_permute follows).  pairs_out nullable.
+bool route_fused_sorts(int cap);
+int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
+                       int norm_topk, int cap, int32_t* pair_offsets, int32_t* pair_expert,
+                       float* pair_weight, int32_t* pairs_out, int32_t* done,
+                       int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
+                       int32_t* gemm_tile_off, hipStream_t s);
 
 size_t permute_ws_bytes(int pair_capacity, int E);
 // gemm_tile_off (nullable): also write the grouped GEMM's per-expert M-tile prefix.

@@ -16,8 +16,9 @@ __global__ __launch_bounds__(64 * KSPLIT) void front_kernel(
     const uint8_t* __restrict__ masked, const int8_t* __restrict__ hist_len,
     const float* __restrict__ c1, const float* __restrict__ c2,
     const int32_t* __restrict__ seq_offsets, const int32_t* __restrict__ active_block, int B,
-    BudgetConsts p, int32_t* __restrict__ k_out) {
+    BudgetConsts p, int32_t* __restrict__ k_out, int32_t* __restrict__ zero_word) {
   const int b = blockIdx.x;
+  if (zero_word != nullptr && b == 0 && threadIdx.x == 0) *zero_word = 0;
   if (b < B) {
     budget_sequence<64 * KSPLIT>(b, block_idx, masked, hist_len, c1, c2, seq_offsets, active_block,
                                  T, p, k_out, nullptr, nullptr);
@@ -35,11 +36,11 @@ int launch_front(const uint16_t* h, const float* w, const float* bias, float* lo
                  int E, const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
                  const float* c1, const float* c2, const int32_t* seq_offsets,
                  const int32_t* active_block, int B, const reflex_alloc_params& prm, int32_t* k_out,
-                 hipStream_t s) {
+                 hipStream_t s, int32_t* zero_word) {
   const int gx = (T + 15) / 16, gy = (E + 15) / 16;
   hipLaunchKernelGGL((front_kernel<16, 1, 16, 4>), dim3(B + gx * gy), dim3(1024), 0, s, h, w, bias,
                      logits, T, d, E, gx, block_idx, masked, hist_len, c1, c2, seq_offsets,
-                     active_block, B, budget_consts(prm), k_out);
+                     active_block, B, budget_consts(prm), k_out, zero_word);
   return launch_status();
 }
 

@@ -359,6 +359,11 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
   f32x16_t acc[2][GM_NT];
   int s = 0;        // flattened step over (tile, K slice), in step with the loading waves
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
+    // a wave's second 32-row block past the expert's last row is skipped: fewer
+    // MFMAs, and less power drawn, on the partly filled tiles of experts with few rows
+    const Tile tt = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
+                                           n_tiles, out_rows);
+    const bool blk1 = tt.row0 + wm * 64 + 32 < tt.row_end;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -394,13 +399,19 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
         }
         // weights as the MFMA's A operand: the accumulator is the transposed tile,
         // so each lane ends up holding 4 consecutive output columns of one row
+        if (blk1) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < GM_NT; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
+                                                                  acc[i][j], 0, 0, 0);
+        } else {
 #pragma unroll
           for (int j = 0; j < GM_NT; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
-                                                                acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);    // MFMAs
+            acc[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][0],
+                                                                acc[0][j], 0, 0, 0);
+        }
       }
     }
     const Tile t = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,

@@ -13,16 +13,12 @@ namespace {
 // ------------------------------------------------------------------------------------
 constexpr int TK_WAVES = 4;
 
-__global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
-    const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
-    int norm_topk, const int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
-    float* __restrict__ pair_weight) {
+// TopK of one token by one wave: the first ki experts of `row` in rank order and
+// their weights, written at pair_expert / pair_weight [o, o + ki).
+__device__ __forceinline__ void topk_token(const float* __restrict__ row, int ki, int E,
+                                           int norm_topk, int o, int32_t* __restrict__ pair_expert,
+                                           float* __restrict__ pair_weight) {
   const int lane = threadIdx.x & 63;
-  const int i = blockIdx.x * TK_WAVES + (threadIdx.x >> 6);
-  if (i >= T) return;
-  const int ki = clamp_count(k[i], k_max);
-  if (ki == 0) return;
-  const float* row = logits + static_cast<size_t>(i) * E;
   uint64_t key[4];
   float val[4];
 #pragma unroll
@@ -60,10 +56,21 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
     den = wave_sum_f32(part);
   }
   if (lane < ki) {
-    const int o = pair_offsets[i] + lane;
-    pair_expert[o] = my_e;
-    pair_weight[o] = expf(my_r - rmax) / den;
+    pair_expert[o + lane] = my_e;
+    pair_weight[o + lane] = expf(my_r - rmax) / den;
   }
+}
+
+__global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
+    const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
+    int norm_topk, const int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
+    float* __restrict__ pair_weight) {
+  const int i = blockIdx.x * TK_WAVES + (threadIdx.x >> 6);
+  if (i >= T) return;
+  const int ki = clamp_count(k[i], k_max);
+  if (ki == 0) return;
+  topk_token(logits + static_cast<size_t>(i) * E, ki, E, norm_topk, pair_offsets[i], pair_expert,
+             pair_weight);
 }
 
 // ------------------------------------------------------------------------------------
@@ -332,7 +339,7 @@ constexpr int PS_THREADS = 1024;
 constexpr int PS_WAVES = PS_THREADS / kWave;
 constexpr int PS_MAX_CAP = 16384;
 
-__global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
+__device__ __forceinline__ void perm_small_run(
     const int32_t* __restrict__ pair_offsets, const int32_t* __restrict__ pair_expert,
     const int32_t* __restrict__ pairs, int T, int cap, int E, int32_t* __restrict__ expert_offsets,
     int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted,
@@ -427,6 +434,76 @@ __global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
   }
 }
 
+__global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
+    const int32_t* __restrict__ pair_offsets, const int32_t* __restrict__ pair_expert,
+    const int32_t* __restrict__ pairs, int T, int cap, int E, int32_t* __restrict__ expert_offsets,
+    int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted,
+    int32_t* __restrict__ gemm_tile_off) {
+  perm_small_run(pair_offsets, pair_expert, pairs, T, cap, E, expert_offsets, sorted_token,
+                 pair_to_sorted, gemm_tile_off);
+}
+
+// ------------------------------------------------------------------------------------
+// Pair offsets, TopK and (for short lists) the permutation in one launch.  Workgroup
+// b owns tokens 16 b .. 16 b + 15, one wave each: it sums the counts of all earlier
+// tokens itself (no separate scan launch), scans its own 16, writes pair_offsets and
+// runs TopK.  With `done` given, the workgroup that finishes last (an agent-scope
+// acquire-release counter; every other workgroup's pairs are then visible to it) sorts
+// the whole list as perm_small_kernel does and resets the counter to zero, which is
+// where the launch before this one left it.
+// ------------------------------------------------------------------------------------
+constexpr int RF_WAVES = 16;
+
+__global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
+    const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
+    int norm_topk, int cap, int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
+    float* __restrict__ pair_weight, int32_t* __restrict__ pairs_out, int32_t* __restrict__ done,
+    int32_t* __restrict__ expert_offsets, int32_t* __restrict__ sorted_token,
+    int32_t* __restrict__ pair_to_sorted, int32_t* __restrict__ gemm_tile_off) {
+  __shared__ int s_before[RF_WAVES], s_cnt[RF_WAVES];
+  __shared__ int s_last;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int t0 = blockIdx.x * RF_WAVES;
+  int part = 0;
+  for (int t = tid; t < t0; t += RF_WAVES * kWave) part += clamp_count(k[t], k_max);
+  part = wave_sum_i32(part);
+  const int i = t0 + wv;
+  const int ki = i < T ? clamp_count(k[i], k_max) : 0;
+  if (lane == 0) {
+    s_before[wv] = part;
+    s_cnt[wv] = ki;
+  }
+  __syncthreads();
+  int base = 0, off = 0, blk = 0;
+#pragma unroll
+  for (int w = 0; w < RF_WAVES; ++w) {
+    base += s_before[w];
+    off += w < wv ? s_cnt[w] : 0;
+    blk += s_cnt[w];
+  }
+  off += base;
+  if (i < T && lane == 0) pair_offsets[i] = off;
+  if (blockIdx.x == gridDim.x - 1 && tid == 0) {     // the last block closes the list
+    pair_offsets[T] = base + blk;
+    if (pairs_out) pairs_out[0] = base + blk;
+  }
+  if (ki > 0)
+    topk_token(logits + static_cast<size_t>(i) * E, ki, E, norm_topk, off, pair_expert, pair_weight);
+  if (done == nullptr) return;
+  // every wave's pair stores acknowledged (vmcnt 0, i.e. in this XCD's L2) before the
+  // barrier, so the counter's agent-scope release by thread 0 writes them all back
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(done, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+             static_cast<int>(gridDim.x) - 1;
+  __syncthreads();
+  if (!s_last) return;
+  perm_small_run(pair_offsets, pair_expert, pair_offsets + T, T, cap, E, expert_offsets,
+                 sorted_token, pair_to_sorted, gemm_tile_off);
+  if (tid == 0) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace
 
 int launch_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
@@ -446,6 +523,20 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
                 hipStream_t s) {
   hipLaunchKernelGGL(topk_kernel, dim3((T + TK_WAVES - 1) / TK_WAVES), dim3(TK_WAVES * kWave), 0, s,
                      logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight);
+  return launch_status();
+}
+
+bool route_fused_sorts(int cap) { return cap <= PS_MAX_CAP; }
+
+int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
+                       int norm_topk, int cap, int32_t* pair_offsets, int32_t* pair_expert,
+                       float* pair_weight, int32_t* pairs_out, int32_t* done,
+                       int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
+                       int32_t* gemm_tile_off, hipStream_t s) {
+  hipLaunchKernelGGL(route_fused_kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave),
+                     0, s, logits, k, T, E, k_max, norm_topk, cap, pair_offsets, pair_expert,
+                     pair_weight, pairs_out, done, expert_offsets, sorted_token, pair_to_sorted,
+                     gemm_tile_off);
   return launch_status();
 }
 

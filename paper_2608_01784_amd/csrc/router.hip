@@ -10,7 +10,9 @@ __global__ __launch_bounds__(64 * KSPLIT) void router_mfma_kernel(const uint16_t
                                                                  const float* __restrict__ w,
                                                                  const float* __restrict__ bias,
                                                                  float* __restrict__ logits, int T,
-                                                                 int d, int E) {
+                                                                 int d, int E,
+                                                                 int32_t* __restrict__ zero_word) {
+  if (zero_word != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *zero_word = 0;
   router_tile<TM, EB, KSPLIT, PF>(blockIdx.x, blockIdx.y, h, w, bias, logits, T, d, E);
 }
 
@@ -57,7 +59,8 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
                                                                 const float* __restrict__ w,
                                                                 const float* __restrict__ bias,
                                                                 float* __restrict__ logits, int T,
-                                                                int d, int E) {
+                                                                int d, int E,
+                                                                int32_t* __restrict__ zero_word) {
   constexpr int TB = TM / 16;                          // token blocks per wave
   constexpr int H_ELEMS = TM * RB_BK;                  // bf16 per h slice
   constexpr int W_ELEMS = RB_TE * RB_BK;               // fp32 per W slice
@@ -70,6 +73,7 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int t0 = blockIdx.x * TM, e0 = blockIdx.y * RB_TE;
   const int nk = d / RB_BK;
+  if (zero_word != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *zero_word = 0;
 
   // copy sources: lane L of an h op fills row 8q + L/8, slot L%8; of a W op row 4q + L/16,
   // slot L%16; rows past T or E repeat the last valid row (their results are not stored)
@@ -148,7 +152,7 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
 }  // namespace
 
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
-                  int d, int E, hipStream_t s) {
+                  int d, int E, hipStream_t s, int32_t* zero_word) {
   // A workgroup's loads all pass through one CU, so tiles are sized to spread the
   // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves;
   // large T uses 64 x 64 tiles so each W_r fragment feeds 4 token blocks.  The
@@ -159,16 +163,16 @@ int launch_router(const uint16_t* h, const float* w, const float* bias, float* l
   const long big_tiles = static_cast<long>((T + 127) / 128) * ((E + RB_TE - 1) / RB_TE);
   if (big_tiles >= 512) {
     hipLaunchKernelGGL((router_big_kernel<128, 2>), dim3((T + 127) / 128, (E + RB_TE - 1) / RB_TE),
-                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E);
+                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else if (T >= 4096) {
     hipLaunchKernelGGL((router_mfma_kernel<64, 4, 4, 2>), dim3((T + 63) / 64, (E + 63) / 64),
-                       dim3(256), 0, s, h, w, bias, logits, T, d, E);
+                       dim3(256), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else if (d % (RT_TK * 16) == 0) {
     hipLaunchKernelGGL((router_mfma_kernel<16, 1, 16, 4>), dim3((T + 15) / 16, (E + 15) / 16),
-                       dim3(1024), 0, s, h, w, bias, logits, T, d, E);
+                       dim3(1024), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else {
     hipLaunchKernelGGL((router_mfma_kernel<16, 1, 4, 4>), dim3((T + 15) / 16, (E + 15) / 16),
-                       dim3(256), 0, s, h, w, bias, logits, T, d, E);
+                       dim3(256), 0, s, h, w, bias, logits, T, d, E, zero_word);
   }
   return launch_status();
 }
