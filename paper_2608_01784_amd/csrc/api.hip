@@ -76,7 +76,7 @@ int check_rule(int rule, float threshold) {
 
 struct Layout {
   size_t logits, k, done, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
-      pair_to_sorted, perm, swiglu, y, shared_act, shared_y, total;
+      pair_to_sorted, perm, route_hist, swiglu, y, shared_act, shared_y, total;
 };
 
 bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
@@ -101,6 +101,7 @@ bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
   L.sorted_token = take(sizeof(int32_t) * cap);
   L.pair_to_sorted = take(sizeof(int32_t) * cap);
   L.perm = take(permute_ws_bytes(static_cast<int>(cap), E));
+  L.route_hist = take(route_fused_sorts(T, E) ? route_hist_bytes(T, E) : 0);
   L.swiglu = take(swiglu_ws_bytes(static_cast<int>(cap), E, f));
   L.y = take(sizeof(uint16_t) * cap * d);
   L.shared_act = fs ? take(swiglu_dense_ws_bytes(T, fs)) : o;
@@ -370,7 +371,7 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   void* gws = at(L.swiglu);
 
   // the fused route kernel's completion counter, zeroed by the router launch
-  int32_t* done = route_fused_sorts(cap) ? static_cast<int32_t*>(at(L.done)) : nullptr;
+  int32_t* done = route_fused_sorts(T, E) ? static_cast<int32_t*>(at(L.done)) : nullptr;
   RFX_TRY(mark(0));
   const int32_t* k = a->k_in;
   // small layers: scores and counts in one launch (independent work side by side)
@@ -400,12 +401,14 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     k = kb;
   }
   RFX_TRY(mark(2));
-  // pair offsets and TopK in one launch (P lives in pair_offsets[T]); short pair lists
-  // are also sorted there, longer ones by the permutation launches.  Either way the
-  // permutation's scan writes the GEMM tile plan at the head of gws.
-  RFX_TRY(launch_route_fused(logits, k, T, E, kcap, a->norm_topk, cap, pair_offsets, pair_expert,
-                             pair_weight, a->pairs_out, done, expert_offsets, sorted_token,
-                             pair_to_sorted, static_cast<int32_t*>(gws), s));
+  // pair offsets and TopK in one launch (P lives in pair_offsets[T]); for layers with
+  // at most RF_HIST_MAX (token block, expert) counts the pairs are also sorted there,
+  // otherwise by the permutation launches.  Either way the sort writes the GEMM tile
+  // plan at the head of gws.
+  RFX_TRY(launch_route_fused(logits, k, T, E, kcap, a->norm_topk, pair_offsets, pair_expert,
+                             pair_weight, a->pairs_out, done, static_cast<int32_t*>(at(L.route_hist)),
+                             expert_offsets, sorted_token, pair_to_sorted,
+                             static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(3));
   if (done == nullptr)
     RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,

@@ -120,13 +120,14 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
                 hipStream_t s);
 
-// Pair offsets + TopK (+ the permutation when route_fused_sorts(cap), with `done` a
-// device word the preceding launch set to zero; else done must be NULL and
-// launch_permute follows).  pairs_out nullable.
-bool route_fused_sorts(int cap);
+// Pair offsets + TopK, and the permutation too when route_fused_sorts(T, E) and `done`
+// is a device word the preceding launch set to zero (hist: route_hist_bytes(T, E) of
+// scratch); else done must be NULL and launch_permute follows.  pairs_out nullable.
+bool route_fused_sorts(int T, int E);
+size_t route_hist_bytes(int T, int E);
 int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
-                       int norm_topk, int cap, int32_t* pair_offsets, int32_t* pair_expert,
-                       float* pair_weight, int32_t* pairs_out, int32_t* done,
+                       int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
+                       float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
                        int32_t* gemm_tile_off, hipStream_t s);
 

@@ -13,25 +13,39 @@ namespace {
 // ------------------------------------------------------------------------------------
 constexpr int TK_WAVES = 4;
 
-// TopK of one token by one wave: the first ki experts of `row` in rank order and
-// their weights, written at pair_expert / pair_weight [o, o + ki).
-__device__ __forceinline__ void topk_token(const float* __restrict__ row, int ki, int E,
-                                           int norm_topk, int o, int32_t* __restrict__ pair_expert,
-                                           float* __restrict__ pair_weight) {
-  const int lane = threadIdx.x & 63;
+// TopK of one token by one wave, in two parts so that the logit loads can be issued
+// early: topk_load reads the token's scores (lane l: experts l, l+64, l+128, l+192),
+// topk_select writes the first ki experts in rank order and their weights at
+// pair_expert / pair_weight [o, o + ki) and returns the lane's expert (-1 past ki).
+struct TopkRow {
   uint64_t key[4];
   float val[4];
+};
+
+__device__ __forceinline__ TopkRow topk_load(const float* __restrict__ row, int E) {
+  const int lane = threadIdx.x & 63;
+  TopkRow r;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + kWave * j;
     if (e < E) {
-      val[j] = row[e];
-      key[j] = (static_cast<uint64_t>(f32_order_key(val[j])) << 32) | (0xffffu - e);
+      r.val[j] = row[e];
+      r.key[j] = (static_cast<uint64_t>(f32_order_key(r.val[j])) << 32) | (0xffffu - e);
     } else {
-      val[j] = 0.0f;
-      key[j] = 0;
+      r.val[j] = 0.0f;
+      r.key[j] = 0;
     }
   }
+  return r;
+}
+
+__device__ __forceinline__ int topk_select(const TopkRow& r, int ki, int E, int norm_topk, int o,
+                                           int32_t* __restrict__ pair_expert,
+                                           float* __restrict__ pair_weight) {
+  const int lane = threadIdx.x & 63;
+  uint64_t key[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) key[x] = r.key[x];
   int my_e = 0;
   float my_r = 0.0f, rmax = 0.0f;
   for (int j = 0; j < ki; ++j) {
@@ -40,10 +54,12 @@ __device__ __forceinline__ void topk_token(const float* __restrict__ row, int ki
     for (int x = 1; x < 4; ++x) best = key[x] > best ? key[x] : best;
     best = wave_max_u64(best);
     const int e = 0xffff - static_cast<int>(best & 0xffffu);
-    const float r = f32_from_order_key(static_cast<uint32_t>(best >> 32));
-    if ((e & 63) == lane) key[e >> 6] = 0;     // consume the winner
-    if (lane == j) { my_e = e; my_r = r; }
-    if (j == 0) rmax = r;
+    const float v = f32_from_order_key(static_cast<uint32_t>(best >> 32));
+#pragma unroll
+    for (int x = 0; x < 4; ++x)        // consume the winner (static indices: registers)
+      key[x] = ((e & 63) == lane && (e >> 6) == x) ? 0 : key[x];
+    if (lane == j) { my_e = e; my_r = v; }
+    if (j == 0) rmax = v;
   }
   float den;
   if (norm_topk) {
@@ -52,13 +68,14 @@ __device__ __forceinline__ void topk_token(const float* __restrict__ row, int ki
     float part = 0.0f;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      if (lane + kWave * j < E) part += expf(val[j] - rmax);
+      if (lane + kWave * j < E) part += expf(r.val[j] - rmax);
     den = wave_sum_f32(part);
   }
   if (lane < ki) {
     pair_expert[o + lane] = my_e;
     pair_weight[o + lane] = expf(my_r - rmax) / den;
   }
+  return lane < ki ? my_e : -1;
 }
 
 __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
@@ -69,8 +86,8 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
   if (i >= T) return;
   const int ki = clamp_count(k[i], k_max);
   if (ki == 0) return;
-  topk_token(logits + static_cast<size_t>(i) * E, ki, E, norm_topk, pair_offsets[i], pair_expert,
-             pair_weight);
+  topk_select(topk_load(logits + static_cast<size_t>(i) * E, E), ki, E, norm_topk, pair_offsets[i],
+              pair_expert, pair_weight);
 }
 
 // ------------------------------------------------------------------------------------
@@ -133,7 +150,9 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void count_rule_kernel(
 #pragma unroll
       for (int x = 0; x < 4; ++x) mine = x == slot ? ex[x] : mine;
       const double m = __shfl(mine, e & 63, kWave);
-      if ((e & 63) == lane) key[slot] = 0;     // consume the winner
+#pragma unroll
+      for (int x = 0; x < 4; ++x)        // consume the winner (static indices: registers)
+        key[x] = ((e & 63) == lane && x == slot) ? 0 : key[x];
       cum += m / den;
       if (cum >= thr) {
         n = j + 1;
@@ -444,30 +463,41 @@ __global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
 }
 
 // ------------------------------------------------------------------------------------
-// Pair offsets, TopK and (for short lists) the permutation in one launch.  Workgroup
+// Pair offsets, TopK and (for small layers) the permutation in one launch.  Workgroup
 // b owns tokens 16 b .. 16 b + 15, one wave each: it sums the counts of all earlier
 // tokens itself (no separate scan launch), scans its own 16, writes pair_offsets and
-// runs TopK.  With `done` given, the workgroup that finishes last (an agent-scope
-// acquire-release counter; every other workgroup's pairs are then visible to it) sorts
-// the whole list as perm_small_kernel does and resets the counter to zero, which is
-// where the launch before this one left it.
+// runs TopK.  With `done` given, it also ranks each of its pairs among the workgroup's
+// pairs of the same expert (an LDS bit mask of the tokens that chose each expert),
+// keeps (token, rank) in pair_to_sorted and its per-expert counts in hist[b][.]; the
+// workgroup that finishes last (agent-scope acquire-release counter, so every other
+// workgroup's pairs are visible to it) turns hist into per-(workgroup, expert) start
+// rows, writes expert_offsets and the GEMM tile plan, and scatters every pair to
+//   expert_offsets[e] + start[b][e] + rank,
+// the same stable (expert, token) order as the permutation kernels.  It then resets the
+// counter to zero, which is where the launch before this one left it.
 // ------------------------------------------------------------------------------------
 constexpr int RF_WAVES = 16;
+constexpr int RF_HIST_MAX = 16384;       // workgroups x experts held in LDS by the last one
 
 __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
-    int norm_topk, int cap, int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
+    int norm_topk, int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
     float* __restrict__ pair_weight, int32_t* __restrict__ pairs_out, int32_t* __restrict__ done,
-    int32_t* __restrict__ expert_offsets, int32_t* __restrict__ sorted_token,
-    int32_t* __restrict__ pair_to_sorted, int32_t* __restrict__ gemm_tile_off) {
+    int32_t* __restrict__ hist, int32_t* __restrict__ expert_offsets,
+    int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted,
+    int32_t* __restrict__ gemm_tile_off) {
   __shared__ int s_before[RF_WAVES], s_cnt[RF_WAVES];
+  __shared__ uint32_t s_mask[REFLEX_MAX_EXPERTS];
   __shared__ int s_last;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int t0 = blockIdx.x * RF_WAVES;
+  for (int e = tid; e < REFLEX_MAX_EXPERTS; e += RF_WAVES * kWave) s_mask[e] = 0;
+  const int i = t0 + wv;
+  // this token's scores are loaded first: their latency overlaps the count prefix
+  const TopkRow row = topk_load(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E);
   int part = 0;
   for (int t = tid; t < t0; t += RF_WAVES * kWave) part += clamp_count(k[t], k_max);
   part = wave_sum_i32(part);
-  const int i = t0 + wv;
   const int ki = i < T ? clamp_count(k[i], k_max) : 0;
   if (lane == 0) {
     s_before[wv] = part;
@@ -487,10 +517,16 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     pair_offsets[T] = base + blk;
     if (pairs_out) pairs_out[0] = base + blk;
   }
-  if (ki > 0)
-    topk_token(logits + static_cast<size_t>(i) * E, ki, E, norm_topk, off, pair_expert, pair_weight);
+  int my_e = -1;
+  if (ki > 0) my_e = topk_select(row, ki, E, norm_topk, off, pair_expert, pair_weight);
   if (done == nullptr) return;
-  // every wave's pair stores acknowledged (vmcnt 0, i.e. in this XCD's L2) before the
+  if (my_e >= 0) atomicOr(&s_mask[my_e], 1u << wv);
+  __syncthreads();
+  if (my_e >= 0)       // (token, rank among this workgroup's tokens that chose my_e)
+    pair_to_sorted[off + lane] = (i << 5) | __popc(s_mask[my_e] & ((1u << wv) - 1u));
+  for (int e = tid; e < E; e += RF_WAVES * kWave)
+    hist[static_cast<size_t>(blockIdx.x) * E + e] = __popc(s_mask[e]);
+  // every wave's stores acknowledged (vmcnt 0, i.e. in this XCD's L2) before the
   // barrier, so the counter's agent-scope release by thread 0 writes them all back
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -499,8 +535,75 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
              static_cast<int>(gridDim.x) - 1;
   __syncthreads();
   if (!s_last) return;
-  perm_small_run(pair_offsets, pair_expert, pair_offsets + T, T, cap, E, expert_offsets,
-                 sorted_token, pair_to_sorted, gemm_tile_off);
+
+  // ---- the last workgroup: start rows and the scatter ----
+  __shared__ int s_tab[RF_HIST_MAX];
+  __shared__ int s_eo[REFLEX_MAX_EXPERTS];
+  __shared__ int s_wave[8];
+  const int G = gridDim.x;
+  for (int x = tid; x < G * E; x += RF_WAVES * kWave) s_tab[x] = hist[x];
+  __syncthreads();
+  // start[w][e] = sum of the column above: one wave scans one expert's column at a time
+  for (int e = wv; e < E; e += RF_WAVES) {
+    int carry = 0;
+    for (int w0 = 0; w0 < G; w0 += kWave) {
+      const int w = w0 + lane;
+      const int c = w < G ? s_tab[w * E + e] : 0;
+      const int inc = wave_inclusive_scan_i32(c, lane);
+      if (w < G) s_tab[w * E + e] = carry + inc - c;
+      carry += __shfl(inc, kWave - 1, kWave);
+    }
+    if (lane == 0) s_eo[e] = carry;        // the expert's total, for the scan below
+  }
+  __syncthreads();
+  const int tot = tid < E ? s_eo[tid] : 0;
+  int incl = 0, tiles = 0, tincl = 0;
+  if (tid < REFLEX_MAX_EXPERTS) {
+    tiles = (tot + kGemmBM - 1) / kGemmBM;
+    incl = wave_inclusive_scan_i32(tot, lane);
+    tincl = wave_inclusive_scan_i32(tiles, lane);
+    if (lane == 63) {
+      s_wave[wv] = incl;
+      s_wave[4 + wv] = tincl;
+    }
+  }
+  __syncthreads();
+  if (tid < E) {
+    int eoff = 0, toff = 0;
+    for (int x = 0; x < wv; ++x) {
+      eoff += s_wave[x];
+      toff += s_wave[4 + x];
+    }
+    const int ebase = eoff + incl - tot;
+    s_eo[tid] = ebase;
+    expert_offsets[tid] = ebase;
+    if (tid == E - 1) expert_offsets[E] = ebase + tot;
+    gemm_tile_off[tid] = toff + tincl - tiles;
+    if (tid == E - 1) gemm_tile_off[E] = toff + tincl;
+  }
+  __syncthreads();
+  // the scatter, RF_BATCH pairs per thread with all their loads issued up front
+  constexpr int RF_BATCH = 4;
+  const int P = pair_offsets[T];
+  for (int p0 = 0; p0 < P; p0 += RF_BATCH * RF_WAVES * kWave) {
+    int v[RF_BATCH], ev[RF_BATCH];
+#pragma unroll
+    for (int j = 0; j < RF_BATCH; ++j) {
+      const int p = p0 + j * RF_WAVES * kWave + tid;
+      v[j] = p < P ? pair_to_sorted[p] : 0;
+      ev[j] = p < P ? pair_expert[p] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < RF_BATCH; ++j) {
+      const int p = p0 + j * RF_WAVES * kWave + tid;
+      if (p >= P) continue;
+      const int e = ev[j] < 0 ? 0 : (ev[j] >= E ? E - 1 : ev[j]);
+      const int t = v[j] >> 5, w = t / RF_WAVES;
+      const int pos = s_eo[e] + s_tab[w * E + e] + (v[j] & 31);
+      sorted_token[pos] = t;
+      pair_to_sorted[p] = pos;
+    }
+  }
   if (tid == 0) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -526,16 +629,22 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
   return launch_status();
 }
 
-bool route_fused_sorts(int cap) { return cap <= PS_MAX_CAP; }
+bool route_fused_sorts(int T, int E) {
+  return static_cast<long>((T + RF_WAVES - 1) / RF_WAVES) * E <= RF_HIST_MAX;
+}
+
+size_t route_hist_bytes(int T, int E) {
+  return align_up(static_cast<size_t>((T + RF_WAVES - 1) / RF_WAVES) * E * sizeof(int32_t));
+}
 
 int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
-                       int norm_topk, int cap, int32_t* pair_offsets, int32_t* pair_expert,
-                       float* pair_weight, int32_t* pairs_out, int32_t* done,
+                       int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
+                       float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
                        int32_t* gemm_tile_off, hipStream_t s) {
   hipLaunchKernelGGL(route_fused_kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave),
-                     0, s, logits, k, T, E, k_max, norm_topk, cap, pair_offsets, pair_expert,
-                     pair_weight, pairs_out, done, expert_offsets, sorted_token, pair_to_sorted,
+                     0, s, logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight,
+                     pairs_out, done, hist, expert_offsets, sorted_token, pair_to_sorted,
                      gemm_tile_off);
   return launch_status();
 }
