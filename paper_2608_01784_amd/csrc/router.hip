@@ -154,19 +154,24 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
                   int d, int E, hipStream_t s, int32_t* zero_word) {
   // A workgroup's loads all pass through one CU, so tiles are sized to spread the
-  // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves;
-  // large T uses 64 x 64 tiles so each W_r fragment feeds 4 token blocks.  The
-  // LDS-staged kernel (128 x 64 tiles, 2-slice ring, two workgroups per CU by LDS) runs
-  // its 64-wide K steps one after another, so it pays only where its grid fills the
-  // GPU at least twice over (measured: half the time of the register kernel at
-  // T = 16384, E = 256; 1.5x its time at T = 8192, E = 64, a grid of 64 workgroups).
+  // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves.  The
+  // LDS-staged kernel runs its 64-wide K steps one after another, so its tiles are made
+  // small enough for its grid to fill the GPU: 128 x 64 tiles where that gives 512 or
+  // more (T = 16384, E = 256: half the time of the register kernel), else 32 x 64 tiles
+  // (T = 4096, E = 256: 33 us against 39 us for 64 x 64 register tiles).  With at most
+  // 64 experts (one expert block) the register kernel with 32-token tiles and K split
+  // over 8 waves is faster still (T = 8192, E = 64: 29 us against 34 us and 38 us for
+  // the LDS kernel and 64 x 64 register tiles; all measured).
   const long big_tiles = static_cast<long>((T + 127) / 128) * ((E + RB_TE - 1) / RB_TE);
   if (big_tiles >= 512) {
     hipLaunchKernelGGL((router_big_kernel<128, 2>), dim3((T + 127) / 128, (E + RB_TE - 1) / RB_TE),
                        dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word);
+  } else if (T >= 4096 && E <= 64 && d % (RT_TK * 8) == 0) {
+    hipLaunchKernelGGL((router_mfma_kernel<32, 4, 8, 2>), dim3((T + 31) / 32, (E + 63) / 64),
+                       dim3(512), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else if (T >= 4096) {
-    hipLaunchKernelGGL((router_mfma_kernel<64, 4, 4, 2>), dim3((T + 63) / 64, (E + 63) / 64),
-                       dim3(256), 0, s, h, w, bias, logits, T, d, E, zero_word);
+    hipLaunchKernelGGL((router_big_kernel<32, 2>), dim3((T + 31) / 32, (E + RB_TE - 1) / RB_TE),
+                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else if (d % (RT_TK * 16) == 0) {
     hipLaunchKernelGGL((router_mfma_kernel<16, 1, 16, 4>), dim3((T + 15) / 16, (E + 15) / 16),
                        dim3(1024), 0, s, h, w, bias, logits, T, d, E, zero_word);

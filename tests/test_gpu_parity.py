@@ -86,12 +86,14 @@ def test_router_logits(torch, name):
 
 
 @pytest.mark.parametrize("T,d,E,with_bias", [(4100, 384, 100, True), (4096, 128, 8, False),
-                                             (9000, 128, 37, False), (16400, 128, 250, False),
-                                             (20000, 256, 200, True)])
+                                             (9000, 128, 37, False), (8200, 512, 60, True),
+                                             (16400, 128, 250, False), (20000, 256, 200, True)])
 def test_router_logits_large_t(torch, T, d, E, with_bias):
-    # T >= 4096: the register kernel with 64 x 64 tiles, and where 128 x 64 tiles number
-    # 512 or more (the last two cases) the LDS-staged kernel; ragged last token tile and
-    # expert counts that are not a multiple of the 64-expert tile
+    # T >= 4096: the LDS-staged kernel with 32 x 64 tiles (first three cases), the
+    # register kernel with 32-token tiles for at most 64 experts and d a multiple of 256
+    # (fourth), the LDS-staged kernel with 128 x 64 tiles where those number 512 or more
+    # (last two); ragged last token tile and expert counts that are not a multiple of
+    # the 64-expert tile
     w = make_fuzz_workload(300 + T % 97, T=T, d=d, E=E, f=64)
     rng = np.random.default_rng([T, d, E])
     bias = (rng.standard_normal(E) * 0.5).astype(np.float32) if with_bias else None
