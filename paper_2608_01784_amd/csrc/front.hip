@@ -37,7 +37,18 @@ int launch_front(const uint16_t* h, const float* w, const float* bias, float* lo
                  const float* c1, const float* c2, const int32_t* seq_offsets,
                  const int32_t* active_block, int B, const reflex_alloc_params& prm, int32_t* k_out,
                  hipStream_t s, int32_t* zero_word) {
-  const int gx = (T + 15) / 16, gy = (E + 15) / 16;
+  // One 1024-thread workgroup fits a CU: with more workgroups than CUs the last ones
+  // wait for a CU to free up and the launch takes two rounds.  32-token score tiles
+  // halve the grid where 16-token tiles would overflow it.
+  const int gy = (E + 15) / 16;
+  if (B + ((T + 15) / 16) * gy > device_cus()) {
+    const int gx = (T + 31) / 32;
+    hipLaunchKernelGGL((front_kernel<32, 1, 16, 4>), dim3(B + gx * gy), dim3(1024), 0, s, h, w,
+                       bias, logits, T, d, E, gx, block_idx, masked, hist_len, c1, c2,
+                       seq_offsets, active_block, B, budget_consts(prm), k_out, zero_word);
+    return launch_status();
+  }
+  const int gx = (T + 15) / 16;
   hipLaunchKernelGGL((front_kernel<16, 1, 16, 4>), dim3(B + gx * gy), dim3(1024), 0, s, h, w, bias,
                      logits, T, d, E, gx, block_idx, masked, hist_len, c1, c2, seq_offsets,
                      active_block, B, budget_consts(prm), k_out, zero_word);

@@ -752,15 +752,7 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* __res
 // One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
 // a multiple of the XCD count.
 int persistent_grid() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
+  const int cus = device_cus();
   return (cus + GM_XCDS - 1) / GM_XCDS * GM_XCDS;
 }
 
