@@ -29,16 +29,23 @@ __global__ __launch_bounds__(256) void combine_kernel(
   p1 = p1 < p0 ? p0 : (p1 > cap ? cap : p1);
   const size_t tok_off = static_cast<size_t>(i) * d;
   for (int v = threadIdx.x * 8; v < d; v += 256 * 8) {
+    // the token's own rows (shared expert, residuals) are loaded first, so they are in
+    // flight with the expert rows; they are still added after them, in the same order
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    const uint4 sv = shared_y ? *reinterpret_cast<const uint4*>(shared_y + tok_off + v) : zero;
+    const uint4 av = res_a ? *reinterpret_cast<const uint4*>(res_a + tok_off + v) : zero;
+    const uint4 bv = res_b ? *reinterpret_cast<const uint4*>(res_b + tok_off + v) : zero;
     float acc[8] = {};
-    for (int p = p0; p < p1; ++p) {
+#pragma unroll 4
+    for (int p = p0; p < p1; ++p) {       // (unrolled: several rows in flight at once)
       int row = pair_to_sorted[p];
       row = row < 0 ? 0 : (row >= cap ? cap - 1 : row);
       add_bf16x8(acc, *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v),
                  pair_weight[p]);
     }
-    if (shared_y) add_bf16x8(acc, *reinterpret_cast<const uint4*>(shared_y + tok_off + v), 1.0f);
-    if (res_a) add_bf16x8(acc, *reinterpret_cast<const uint4*>(res_a + tok_off + v), 1.0f);
-    if (res_b) add_bf16x8(acc, *reinterpret_cast<const uint4*>(res_b + tok_off + v), 1.0f);
+    if (shared_y) add_bf16x8(acc, sv, 1.0f);
+    if (res_a) add_bf16x8(acc, av, 1.0f);
+    if (res_b) add_bf16x8(acc, bv, 1.0f);
     uint4 o;
     o.x = pack_bf16x2(acc[0], acc[1]);
     o.y = pack_bf16x2(acc[2], acc[3]);

@@ -25,16 +25,20 @@ struct TopkRow {
 __device__ __forceinline__ TopkRow topk_load(const float* __restrict__ row, int E) {
   const int lane = threadIdx.x & 63;
   TopkRow r;
+  // four unconditional loads (lanes past E read expert E-1 and discard it), all in
+  // flight together rather than one guarded load and wait at a time
+  float v[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + kWave * j;
-    if (e < E) {
-      r.val[j] = row[e];
-      r.key[j] = (static_cast<uint64_t>(f32_order_key(r.val[j])) << 32) | (0xffffu - e);
-    } else {
-      r.val[j] = 0.0f;
-      r.key[j] = 0;
-    }
+    v[j] = row[e < E ? e : E - 1];
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + kWave * j;
+    const bool ok = e < E;
+    r.val[j] = ok ? v[j] : 0.0f;
+    r.key[j] = ok ? (static_cast<uint64_t>(f32_order_key(v[j])) << 32) | (0xffffu - e) : 0;
   }
   return r;
 }
@@ -113,10 +117,16 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void count_rule_kernel(
   uint64_t key[4];
   float val[4];
   uint64_t best = 0;
+  float v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {     // unconditional loads, all in flight together
+    const int e = lane + kWave * j;
+    v[j] = row[e < E ? e : E - 1];
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + kWave * j;
-    val[j] = e < E ? row[e] : 0.0f;
+    val[j] = e < E ? v[j] : 0.0f;
     key[j] = e < E ? (static_cast<uint64_t>(f32_order_key(val[j])) << 32) | (0xffffu - e) : 0;
     best = key[j] > best ? key[j] : best;
   }
@@ -495,7 +505,8 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   const int i = t0 + wv;
   // this token's scores are loaded first: their latency overlaps the count prefix
   const TopkRow row = topk_load(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E);
-  int part = 0;
+  int part = 0;     // (unrolled so that several count loads are in flight at once)
+#pragma unroll 8
   for (int t = tid; t < t0; t += RF_WAVES * kWave) part += clamp_count(k[t], k_max);
   part = wave_sum_i32(part);
   const int ki = i < T ? clamp_count(k[i], k_max) : 0;
@@ -541,6 +552,7 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   __shared__ int s_eo[REFLEX_MAX_EXPERTS];
   __shared__ int s_wave[8];
   const int G = gridDim.x;
+#pragma unroll 8
   for (int x = tid; x < G * E; x += RF_WAVES * kWave) s_tab[x] = hist[x];
   __syncthreads();
   // start[w][e] = sum of the column above: one wave scans one expert's column at a time
