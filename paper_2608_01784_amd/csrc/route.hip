@@ -237,8 +237,10 @@ __global__ __launch_bounds__(PM_SCAN_THREADS) void perm_scan_kernel(
   const int per = (n_tiles + 3) / 4;
   const int tb = q * per, te = min(n_tiles, tb + per);
   int n = 0;
-  if (e < E)
-    for (int t = tb; t < te; ++t) n += hist[static_cast<size_t>(t) * E + e];
+  if (e < E) {
+#pragma unroll 8
+    for (int t = tb; t < te; ++t) n += hist[static_cast<size_t>(t) * E + e];   // 8 loads in flight
+  }
   s_part[q][e] = n;
   __syncthreads();
   int tot = 0, incl = 0, tiles = 0, tincl = 0;
@@ -274,22 +276,49 @@ __global__ __launch_bounds__(PM_SCAN_THREADS) void perm_scan_kernel(
   if (e < E) {
     int run = s_base[e];
     for (int qq = 0; qq < q; ++qq) run += s_part[qq][e];
-    for (int t = tb; t < te; ++t) {
-      const size_t x = static_cast<size_t>(t) * E + e;
-      const int c = hist[x];
-      hist[x] = run;
-      run += c;
+    // start rows of the group's tiles, in batches of 8 whose counts are loaded together
+    for (int t0 = tb; t0 < te; t0 += 8) {
+      int c[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {       // unconditional loads (clamped), then selects
+        const int tt = t0 + j < te ? t0 + j : te - 1;
+        c[j] = hist[static_cast<size_t>(tt) * E + e];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) c[j] = t0 + j < te ? c[j] : 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (t0 + j < te) hist[static_cast<size_t>(t0 + j) * E + e] = run;
+        run += c[j];
+      }
     }
   }
 }
 
-// Largest token i in [lo, hi] with pair_offsets[i] <= p: the token that owns pair p.
-__device__ __forceinline__ int owner_token(const int32_t* __restrict__ off, int lo, int hi, int p) {
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= p) lo = mid; else hi = mid - 1;
+// The tokens that own pairs pa and pb: the largest i in [0, T) with off[i] <= p (off is
+// the nondecreasing pair-offset scan), for both at once, by the whole workgroup.  Each
+// round samples 256 evenly spaced entries of the current range in one load per thread
+// and keeps the bracket the count of samples <= p points to: two rounds of dependent
+// loads for up to 65536 tokens instead of a 16-step binary search by one thread.
+__device__ __forceinline__ void owner_tokens(const int32_t* __restrict__ off, int T, int pa,
+                                             int pb, int* s_out) {
+  int lo_a = 0, n_a = T, lo_b = 0, n_b = T;      // candidate ranges [lo, lo + n)
+  while (n_a > 1 || n_b > 1) {                   // uniform across the workgroup
+    const int st_a = (n_a + PM_THREADS - 1) / PM_THREADS, st_b = (n_b + PM_THREADS - 1) / PM_THREADS;
+    const int ia = threadIdx.x * st_a, ib = threadIdx.x * st_b;
+    const bool fa = ia < n_a && off[lo_a + ia] <= pa;
+    const bool fb = ib < n_b && off[lo_b + ib] <= pb;
+    const int ca = __syncthreads_count(fa), cb = __syncthreads_count(fb);
+    const int ka = ca > 0 ? ca - 1 : 0, kb = cb > 0 ? cb - 1 : 0;   // last sample <= p
+    lo_a += ka * st_a;
+    n_a = min(st_a, n_a - ka * st_a);
+    lo_b += kb * st_b;
+    n_b = min(st_b, n_b - kb * st_b);
   }
-  return lo;
+  if (threadIdx.x == 0) {
+    s_out[0] = lo_a;
+    s_out[1] = lo_b;
+  }
 }
 
 __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
@@ -310,7 +339,7 @@ __global__ __launch_bounds__(PM_THREADS) void perm_scatter_kernel(
 #pragma unroll
     for (int w = 0; w < PM_THREADS / kWave; ++w) wcnt[w][e] = 0;
   }
-  if (tid < 2) s_tok[tid] = owner_token(pair_offsets, 0, T - 1, tid == 0 ? begin : end - 1);
+  owner_tokens(pair_offsets, T, begin, end - 1, s_tok);
   __syncthreads();
   // owning token of every pair of the tile
   for (int i = s_tok[0] + tid; i <= s_tok[1]; i += PM_THREADS) {
