@@ -598,3 +598,53 @@ def test_packed_weights_give_bitwise_identical_layer(torch, case):
         outs.append(bf16_bits(lay.forward(to_device(w.h), TokenState(**state_tensors(w)))))
         torch.cuda.synchronize()
     assert np.array_equal(outs[0], outs[1])
+
+
+def _fuzz_layer(torch, w, k_in=None):
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    dw = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()), "w_down": to_device(w.w_down()),
+          "w_router": to_device(w.w_router()),
+          "router_bias": None if w.router_bias is None else to_device(w.router_bias)}
+    lay = MoELayer(w.T, w.d, ExpertWeights(**dw), w.params)
+    return lay, TokenState(**state_tensors(w))
+
+
+def _fuzz_ref(w, logits, k):
+    route = oracle.topk_route(logits, k)
+    wg, wu, wd = w.w_gate(), w.w_up(), w.w_down()
+    return oracle.moe_layer(w.h, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
+
+
+@pytest.mark.parametrize("T", [4096, 4112])
+def test_fused_route_sort_limit(torch, T):
+    # the fused forward sorts the pairs inside its route launch while (16-token blocks) x
+    # experts <= 16384 (T = 4096, E = 64: exactly the limit, 256 workgroups) and with the
+    # permutation launches above it (T = 4112)
+    w = make_fuzz_workload(120, T=T, d=128, E=64, f=64, k_max=12)
+    lay, st = _fuzz_layer(torch, w)
+    out = oracle.bf16_to_f64(bf16_bits(lay.forward(to_device(w.h), st)))
+    torch.cuda.synchronize()
+    k = lay.k.cpu().numpy()
+    assert np.array_equal(k, oracle_budget(w).k)
+    assert int(lay.pairs.item()) == int(k.sum())
+    ref = _fuzz_ref(w, lay.logits.cpu().numpy().astype(np.float64), k)
+    layer_tolerance_check(out, ref, f"route sort limit T={T}")
+
+
+def test_fused_consecutive_calls_and_no_pairs(torch):
+    # the route launch's completion counter is re-armed by every forward: three forwards
+    # in a row on one workspace, with caller counts that differ (the last one all zero,
+    # P = 0: an all-zero output), each checked against the oracle
+    w = make_fuzz_workload(121, T=700, d=256, E=16, f=128, k_max=6)
+    lay, st = _fuzz_layer(torch, w)
+    rng = np.random.default_rng(7)
+    for n, k in enumerate([rng.integers(0, 7, w.T), rng.integers(0, 3, w.T), np.zeros(w.T, np.int64)]):
+        out = oracle.bf16_to_f64(bf16_bits(lay.forward(to_device(w.h), st,
+                                                       k_in=to_device(k.astype(np.int32)))))
+        torch.cuda.synchronize()
+        assert int(lay.pairs.item()) == int(k.sum()), n
+        if k.sum() == 0:
+            assert np.all(out == 0.0)
+            continue
+        ref = _fuzz_ref(w, lay.logits.cpu().numpy().astype(np.float64), k)
+        layer_tolerance_check(out, ref, f"consecutive call {n}")
