@@ -177,53 +177,81 @@ __device__ __forceinline__ void lds_barrier() {
 // Epilogue of one compute wave: its 64 x (32 NT) accumulator block (2 x NT MFMA
 // tiles, weights as the A operand) to bf16 rows of `out`.  Lane l, register r holds
 // output row l % 32 (a pair row) and column 8 (r/4) + 4 (l/32) + r%4 of its 32 x 32
-// block, so registers 4g..4g+3 are 4 consecutive columns: one 8-byte store each.
-// UP: sub-tiles j and j + NT/2 hold gate and up of the same columns and the store
-// is SiLU(g) u.  Rows at or past the tile's row_end are skipped; N is a multiple of
-// 64, so a group of 4 columns is wholly inside a partial last N tile or wholly past it.
+// block.  Stored as it lies, one instruction would write 8 bytes to each of 32 rows;
+// instead each 32 x 32 bf16 block goes through the wave's staging buffer in LDS and
+// comes back with 4 lanes per row, so each store instruction writes 16 rows of 64
+// contiguous bytes (a quarter of the write requests).  UP: sub-tiles j and j + NT/2
+// hold gate and up of the same columns and the stored value is SiLU(g) u.  Rows at
+// or past the tile's row_end are skipped; N is a multiple of 64, so a group of 8
+// columns is wholly inside a partial last N tile or wholly past it.
+//
+// The staging accesses are inline assembly: the compiler cannot tell that the buffer
+// does not alias the ring the direct-to-LDS copies write, and would wait for the next
+// slice's copies (issued before the epilogue) before touching it.
+constexpr int ST_LD = 40;                 // staging row pitch (elements): 80 B, 16 B aligned
+constexpr int ST_ELEMS = 32 * ST_LD;      // one wave's staging buffer
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 template <bool UP, int NT>
 __device__ __forceinline__ void store_wave_tile(const f32x16_t (&acc)[2][NT], const Tile& t,
                                                 int row_in_tile, int col0, int N_out,
-                                                uint16_t* __restrict__ out) {
-  const int lane = threadIdx.x & 63, ccol = 4 * (lane >> 5);
+                                                uint16_t* __restrict__ out, uint16_t* stage) {
+  const int lane = threadIdx.x & 63;
+  // LDS byte offsets: a generic pointer to LDS carries the offset in its low 32 bits
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(stage));
+  const uint32_t wr = base + ((lane & 31) * ST_LD + 4 * (lane >> 5)) * 2;
+  const uint32_t rd = base + ((lane >> 2) * ST_LD + 8 * (lane & 3)) * 2;
+  constexpr int NB = UP ? NT / 2 : NT;     // 32-column output blocks per 32 rows
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int grow = t.row0 + row_in_tile + 32 * i + (lane & 31);
-    if (grow >= t.row_end) continue;
-    uint16_t* orow = out + static_cast<size_t>(grow) * N_out + t.n0;
-    if (UP) {
+    const int rbase = t.row0 + row_in_tile + 32 * i + (lane >> 2);
 #pragma unroll
-      for (int j = 0; j < NT / 2; ++j) {
+    for (int jb = 0; jb < NB; ++jb) {
+      u32x2_t v[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = col0 + 32 * j + 8 * g + ccol;
-          float a4[4];
+      for (int g = 0; g < 4; ++g) {
+        float a4[4];
 #pragma unroll
-          for (int h = 0; h < 4; ++h) {     // SiLU(g) u = g u / (1 + e^-g), e^x = 2^(x log2 e)
-            const float gg = acc[i][j][4 * g + h], uu = acc[i][j + NT / 2][4 * g + h];
+        for (int h = 0; h < 4; ++h) {
+          if (UP) {     // SiLU(g) u = g u / (1 + e^-g), e^x = 2^(x log2 e)
+            const float gg = acc[i][jb][4 * g + h], uu = acc[i][jb + NT / 2][4 * g + h];
             const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
             a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
+          } else {
+            a4[h] = acc[i][jb][4 * g + h];
           }
-          if (t.n0 + c < N_out)
-            *reinterpret_cast<uint2*>(orow + c) =
-                make_uint2(pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3]));
         }
+        v[g] = u32x2_t{pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3])};
       }
-    } else {
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = col0 + 32 * j + 8 * g + ccol;
-          const f32x16_t& a = acc[i][j];
-          if (t.n0 + c < N_out)
-            *reinterpret_cast<uint2*>(orow + c) =
-                make_uint2(pack_bf16x2(a[4 * g], a[4 * g + 1]), pack_bf16x2(a[4 * g + 2], a[4 * g + 3]));
-        }
+      u32x4_t r0, r1;
+      // write the block (row l%32, columns 8g + 4(l/32) ..+3), read rows l/4 and
+      // 16 + l/4 (columns 8 (l%4) ..+7); the wait ends the reads before the next
+      // block overwrites the buffer
+      asm volatile(
+          "ds_write_b64 %2, %4\n\t"
+          "ds_write_b64 %2, %5 offset:16\n\t"
+          "ds_write_b64 %2, %6 offset:32\n\t"
+          "ds_write_b64 %2, %7 offset:48\n\t"
+          "ds_read_b128 %0, %3\n\t"
+          "ds_read_b128 %1, %3 offset:1280\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(r0), "=&v"(r1)
+          : "v"(wr), "v"(rd), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3])
+          : "memory");
+      const int col = t.n0 + col0 + 32 * jb + 8 * (lane & 3);
+      if (col < N_out) {
+        if (rbase < t.row_end)
+          *reinterpret_cast<u32x4_t*>(out + static_cast<size_t>(rbase) * N_out + col) = r0;
+        if (rbase + 16 < t.row_end)
+          *reinterpret_cast<u32x4_t*>(out + static_cast<size_t>(rbase + 16) * N_out + col) = r1;
       }
     }
   }
 }
+
+static_assert(GM_LDS + 8 * (REFLEX_MAX_EXPERTS + 1) + GM_CW * ST_ELEMS * 2 <= 160 * 1024,
+              "128-row ring + staging");
 
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
@@ -242,6 +270,7 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
   const int n_tiles = (N_out + BN - 1) / BN;     // the last N tile may be partial
   // the tile plan and expert row offsets, copied to LDS once for the tile decodes
   __shared__ int s_tile_off[REFLEX_MAX_EXPERTS + 1], s_eo[REFLEX_MAX_EXPERTS + 1];
+  __shared__ __attribute__((aligned(16))) uint16_t s_stage[GM_CW][ST_ELEMS];
   if (dense_M < 0) {
     for (int e = threadIdx.x; e <= E; e += blockDim.x) {
       s_tile_off[e] = tile_off[e];
@@ -424,7 +453,8 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     const Tile t = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
                                           n_tiles, out_rows);
     store_wave_tile<UP, GM_NT>(acc, t, wm * 64,
-                               UP ? wn * (GM_BROWS / 2 / GM_WN) : wn * (GM_BROWS / GM_WN), N_out, out);
+                               UP ? wn * (GM_BROWS / 2 / GM_WN) : wn * (GM_BROWS / GM_WN), N_out, out,
+                               s_stage[wv]);
   }
 }
 
@@ -466,7 +496,7 @@ constexpr int TL_B_OPS = GM_BROWS / TL_ROWS_PER_OP / TL_WAVES;
 constexpr size_t TL_LDS = size_t(TL_STAGES) * TL_STAGE_ELEMS * sizeof(uint16_t);
 static_assert(TL_BK == 32 || TL_BK == 64, "tall BK");
 static_assert(GM_BROWS == 256, "tall tiles: two wave columns of 128 weight rows");
-static_assert(TL_LDS + 8192 <= 160 * 1024, "tall LDS ring");
+static_assert(TL_LDS + 8192 + TL_WAVES * ST_ELEMS * 2 <= 160 * 1024, "tall LDS ring + staging");
 
 template <bool UP>
 __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
@@ -482,6 +512,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   // expert row offsets and the per-expert prefix of 256-row tiles
   __shared__ int s_tile_off[REFLEX_MAX_EXPERTS + 1], s_eo[REFLEX_MAX_EXPERTS + 1];
   __shared__ int s_part[TL_WAVES];
+  __shared__ __attribute__((aligned(16))) uint16_t s_stage[TL_WAVES][ST_ELEMS];
   for (int e = tid; e <= E; e += TL_THREADS) s_eo[e] = expert_offsets[e];
   __syncthreads();
   {
@@ -682,7 +713,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     }
     if (active)
       store_wave_tile<UP, TL_NT>(acc, t, wm * 64, UP ? wn * (GM_BROWS / 4) : wn * (GM_BROWS / 2),
-                                 N_out, out);
+                                 N_out, out, s_stage[wave]);
   }
   waitcnt_vm<0>();     // the last (unused) copy lands before the workgroup's LDS is released
 }
