@@ -30,35 +30,106 @@ RFX_DEVICE uint32_t pack_bf16x2(float lo, float hi) {
 RFX_DEVICE uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
 
 // ---- wave64 reductions ----------------------------------------------------------------
+// Built from DPP lane moves within 16-lane rows and the row swaps of v_permlane16_swap /
+// v_permlane32_swap, all VALU: no LDS round trip per step, as a shuffle through
+// ds_bpermute would take.  Every step pairs lanes symmetrically, so an all-reduce leaves
+// the bit-identical result in every lane (floating-point sums included).
+template <int CTRL>
+RFX_DEVICE uint32_t dpp_u32(uint32_t v) {     // a lane move that has a source in every lane
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // lane i <-> 7 - i within 8 lanes
+constexpr int kDppMirror = 0x140;       // lane i <-> 15 - i within a row
+
+// The value of the lane in the partner row (rows 0<->1, 2<->3) and in the partner half
+// (lanes 0-31 <-> 32-63).  With both operands x, permlane16_swap returns rows
+// (x0, x0, x2, x2) and (x1, x1, x3, x3): the lane's own row in one, the partner's in the
+// other; a symmetric combine of the two needs not know which.
+RFX_DEVICE void rows_swap16(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+RFX_DEVICE void rows_swap32(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+
 RFX_DEVICE int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  uint32_t x = static_cast<uint32_t>(v), a, b;
+  x += dpp_u32<kDppXor1>(x);
+  x += dpp_u32<kDppXor2>(x);
+  x += dpp_u32<kDppHalfMirror>(x);
+  x += dpp_u32<kDppMirror>(x);
+  rows_swap16(x, a, b);
+  x = a + b;
+  rows_swap32(x, a, b);
+  return static_cast<int>(a + b);
 }
 
 RFX_DEVICE float wave_sum_f32(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  uint32_t a, b;
+  v += __uint_as_float(dpp_u32<kDppXor1>(__float_as_uint(v)));
+  v += __uint_as_float(dpp_u32<kDppXor2>(__float_as_uint(v)));
+  v += __uint_as_float(dpp_u32<kDppHalfMirror>(__float_as_uint(v)));
+  v += __uint_as_float(dpp_u32<kDppMirror>(__float_as_uint(v)));
+  rows_swap16(__float_as_uint(v), a, b);
+  v = __uint_as_float(a) + __uint_as_float(b);
+  rows_swap32(__float_as_uint(v), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+
+template <int CTRL>
+RFX_DEVICE uint64_t max_dpp_u64(uint64_t v) {
+  const uint64_t w = (static_cast<uint64_t>(dpp_u32<CTRL>(static_cast<uint32_t>(v >> 32))) << 32) |
+                     dpp_u32<CTRL>(static_cast<uint32_t>(v));
+  return w > v ? w : v;
 }
 
 RFX_DEVICE uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t w = __shfl_xor(v, o, kWave);
-    v = w > v ? w : v;
-  }
-  return v;
+  v = max_dpp_u64<kDppXor1>(v);
+  v = max_dpp_u64<kDppXor2>(v);
+  v = max_dpp_u64<kDppHalfMirror>(v);
+  v = max_dpp_u64<kDppMirror>(v);
+  uint32_t a_lo, b_lo, a_hi, b_hi;
+  rows_swap16(static_cast<uint32_t>(v), a_lo, b_lo);
+  rows_swap16(static_cast<uint32_t>(v >> 32), a_hi, b_hi);
+  uint64_t a = (static_cast<uint64_t>(a_hi) << 32) | a_lo, b = (static_cast<uint64_t>(b_hi) << 32) | b_lo;
+  v = a > b ? a : b;
+  rows_swap32(static_cast<uint32_t>(v), a_lo, b_lo);
+  rows_swap32(static_cast<uint32_t>(v >> 32), a_hi, b_hi);
+  a = (static_cast<uint64_t>(a_hi) << 32) | a_lo;
+  b = (static_cast<uint64_t>(b_hi) << 32) | b_lo;
+  return a > b ? a : b;
 }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
-RFX_DEVICE int wave_inclusive_scan_i32(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    int w = __shfl_up(v, o, kWave);
-    if (lane >= o) v += w;
-  }
-  return v;
+RFX_DEVICE uint32_t wave_max_u32(uint32_t v) {
+  uint32_t a, b;
+  v = max(v, dpp_u32<kDppXor1>(v));
+  v = max(v, dpp_u32<kDppXor2>(v));
+  v = max(v, dpp_u32<kDppHalfMirror>(v));
+  v = max(v, dpp_u32<kDppMirror>(v));
+  rows_swap16(v, a, b);
+  v = max(a, b);
+  rows_swap32(v, a, b);
+  return max(a, b);
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave: shifts by 1, 2, 4, 8 within each
+// 16-lane row (lanes with no source add 0), then the last lane of row 0 added to row 1
+// and of row 2 to row 3 (row_bcast:15), then lane 31 added to rows 2 and 3 (row_bcast:31).
+RFX_DEVICE int wave_inclusive_scan_i32(int v, int /*lane*/) {
+  int x = v;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15, rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31, rows 2, 3
+  return x;
 }
 
 // Order-preserving map of fp32 to uint32 (larger float -> larger key), with

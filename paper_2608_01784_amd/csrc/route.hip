@@ -14,54 +14,72 @@ namespace {
 constexpr int TK_WAVES = 4;
 
 // TopK of one token by one wave, in two parts so that the logit loads can be issued
-// early: topk_load reads the token's scores (lane l: experts l, l+64, l+128, l+192),
-// topk_select writes the first ki experts in rank order and their weights at
-// pair_expert / pair_weight [o, o + ki) and returns the lane's expert (-1 past ki).
+// early: topk_load reads the token's scores (lane l: experts l, l+64, ... over NX
+// slots of 64), topk_select writes the first ki experts in rank order and their
+// weights at pair_expert / pair_weight [o, o + ki) and returns the lane's expert (-1
+// past ki).  Ranking is by score, ties to the lower expert index.  Each round takes the
+// wave maximum of the 32-bit order keys and resolves ties with ballots: the first slot
+// holding the maximum, then its lowest lane, is the lowest expert index.  Consumed
+// experts and lanes past E hold key 0, below every finite score's key.
+template <int NX>
 struct TopkRow {
-  uint64_t key[4];
-  float val[4];
+  uint32_t key[NX];
+  float val[NX];
 };
 
-__device__ __forceinline__ TopkRow topk_load(const float* __restrict__ row, int E) {
+template <int NX>
+__device__ __forceinline__ TopkRow<NX> topk_load(const float* __restrict__ row, int E) {
   const int lane = threadIdx.x & 63;
-  TopkRow r;
-  // four unconditional loads (lanes past E read expert E-1 and discard it), all in
-  // flight together rather than one guarded load and wait at a time
-  float v[4];
+  TopkRow<NX> r;
+  // unconditional loads (lanes past E read expert E-1 and discard it), all in flight
+  // together rather than one guarded load and wait at a time
+  float v[NX];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < NX; ++j) {
     const int e = lane + kWave * j;
     v[j] = row[e < E ? e : E - 1];
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + kWave * j;
-    const bool ok = e < E;
+  for (int j = 0; j < NX; ++j) {
+    const bool ok = lane + kWave * j < E;
     r.val[j] = ok ? v[j] : 0.0f;
-    r.key[j] = ok ? (static_cast<uint64_t>(f32_order_key(v[j])) << 32) | (0xffffu - e) : 0;
+    r.key[j] = ok ? f32_order_key(v[j]) : 0u;
   }
   return r;
 }
 
-__device__ __forceinline__ int topk_select(const TopkRow& r, int ki, int E, int norm_topk, int o,
-                                           int32_t* __restrict__ pair_expert,
+template <int NX>
+__device__ __forceinline__ int topk_select(const TopkRow<NX>& r, int ki, int E, int norm_topk,
+                                           int o, int32_t* __restrict__ pair_expert,
                                            float* __restrict__ pair_weight) {
   const int lane = threadIdx.x & 63;
-  uint64_t key[4];
+  uint32_t key[NX];
 #pragma unroll
-  for (int x = 0; x < 4; ++x) key[x] = r.key[x];
+  for (int x = 0; x < NX; ++x) key[x] = r.key[x];
   int my_e = 0;
   float my_r = 0.0f, rmax = 0.0f;
   for (int j = 0; j < ki; ++j) {
-    uint64_t best = key[0];
+    uint32_t best = key[0];
 #pragma unroll
-    for (int x = 1; x < 4; ++x) best = key[x] > best ? key[x] : best;
-    best = wave_max_u64(best);
-    const int e = 0xffff - static_cast<int>(best & 0xffffu);
-    const float v = f32_from_order_key(static_cast<uint32_t>(best >> 32));
+    for (int x = 1; x < NX; ++x) best = max(best, key[x]);
+    best = wave_max_u32(best);
+    // the winner: the first slot with a lane at the maximum, its lowest such lane
+    int wx = 0;
+    uint64_t wm = __ballot(key[0] == best);
 #pragma unroll
-    for (int x = 0; x < 4; ++x)        // consume the winner (static indices: registers)
-      key[x] = ((e & 63) == lane && (e >> 6) == x) ? 0 : key[x];
+    for (int x = 1; x < NX; ++x) {
+      const uint64_t m = __ballot(key[x] == best);
+      if (wm == 0) {
+        wm = m;
+        wx = x;
+      }
+    }
+    const int wl = __builtin_ctzll(wm);
+    const int e = wl + kWave * wx;
+    const float v = f32_from_order_key(best);
+#pragma unroll
+    for (int x = 0; x < NX; ++x)        // consume the winner (static indices: registers)
+      key[x] = (lane == wl && x == wx) ? 0u : key[x];
     if (lane == j) { my_e = e; my_r = v; }
     if (j == 0) rmax = v;
   }
@@ -71,7 +89,7 @@ __device__ __forceinline__ int topk_select(const TopkRow& r, int ki, int E, int 
   } else {
     float part = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NX; ++j)
       if (lane + kWave * j < E) part += expf(r.val[j] - rmax);
     den = wave_sum_f32(part);
   }
@@ -82,6 +100,10 @@ __device__ __forceinline__ int topk_select(const TopkRow& r, int ki, int E, int 
   return lane < ki ? my_e : -1;
 }
 
+// Slots of 64 experts per lane for E experts.
+inline int topk_slots(int E) { return (E + kWave - 1) / kWave; }
+
+template <int NX>
 __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
     int norm_topk, const int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
@@ -90,7 +112,7 @@ __global__ __launch_bounds__(TK_WAVES * kWave) void topk_kernel(
   if (i >= T) return;
   const int ki = clamp_count(k[i], k_max);
   if (ki == 0) return;
-  topk_select(topk_load(logits + static_cast<size_t>(i) * E, E), ki, E, norm_topk, pair_offsets[i],
+  topk_select<NX>(topk_load<NX>(logits + static_cast<size_t>(i) * E, E), ki, E, norm_topk, pair_offsets[i],
               pair_expert, pair_weight);
 }
 
@@ -518,6 +540,7 @@ __global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
 constexpr int RF_WAVES = 16;
 constexpr int RF_HIST_MAX = 16384;       // workgroups x experts held in LDS by the last one
 
+template <int NX>
 __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
     int norm_topk, int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
@@ -533,7 +556,7 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   for (int e = tid; e < REFLEX_MAX_EXPERTS; e += RF_WAVES * kWave) s_mask[e] = 0;
   const int i = t0 + wv;
   // this token's scores are loaded first: their latency overlaps the count prefix
-  const TopkRow row = topk_load(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E);
+  const TopkRow<NX> row = topk_load<NX>(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E);
   int part = 0;     // (unrolled so that several count loads are in flight at once)
 #pragma unroll 8
   for (int t = tid; t < t0; t += RF_WAVES * kWave) part += clamp_count(k[t], k_max);
@@ -558,7 +581,7 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     if (pairs_out) pairs_out[0] = base + blk;
   }
   int my_e = -1;
-  if (ki > 0) my_e = topk_select(row, ki, E, norm_topk, off, pair_expert, pair_weight);
+  if (ki > 0) my_e = topk_select<NX>(row, ki, E, norm_topk, off, pair_expert, pair_weight);
   if (done == nullptr) return;
   if (my_e >= 0) atomicOr(&s_mask[my_e], 1u << wv);
   __syncthreads();
@@ -577,24 +600,60 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   if (!s_last) return;
 
   // ---- the last workgroup: start rows and the scatter ----
+  constexpr int RF_BATCH = 8;                       // pairs per thread per scatter pass
+  constexpr int RF_PASS = RF_BATCH * RF_WAVES * kWave;
   __shared__ int s_tab[RF_HIST_MAX];
+  __shared__ int s_part[RF_WAVES][REFLEX_MAX_EXPERTS];
   __shared__ int s_eo[REFLEX_MAX_EXPERTS];
   __shared__ int s_wave[8];
-  const int G = gridDim.x;
-#pragma unroll 8
-  for (int x = tid; x < G * E; x += RF_WAVES * kWave) s_tab[x] = hist[x];
-  __syncthreads();
-  // start[w][e] = sum of the column above: one wave scans one expert's column at a time
-  for (int e = wv; e < E; e += RF_WAVES) {
-    int carry = 0;
-    for (int w0 = 0; w0 < G; w0 += kWave) {
-      const int w = w0 + lane;
-      const int c = w < G ? s_tab[w * E + e] : 0;
-      const int inc = wave_inclusive_scan_i32(c, lane);
-      if (w < G) s_tab[w * E + e] = carry + inc - c;
-      carry += __shfl(inc, kWave - 1, kWave);
+  constexpr int RF_THREADS = RF_WAVES * kWave;
+  constexpr int RF_TAB_PT = RF_HIST_MAX / RF_THREADS;     // table words per thread, at most
+  const int G = gridDim.x, n_tab = G * E;
+  // the whole table's loads in flight at once (a uniform branch skips the unused
+  // slices), then the pair count's, then one wait
+  int hv[RF_TAB_PT];
+#pragma unroll
+  for (int j = 0; j < RF_TAB_PT; ++j)
+    if (j * RF_THREADS < n_tab) hv[j] = hist[min(tid + j * RF_THREADS, n_tab - 1)];
+  const int P = pair_offsets[T];
+#pragma unroll
+  for (int j = 0; j < RF_TAB_PT; ++j)
+    if (j * RF_THREADS < n_tab && tid + j * RF_THREADS < n_tab) s_tab[tid + j * RF_THREADS] = hv[j];
+  // the first pass's scatter inputs do not depend on the start rows: their loads go
+  // out now and their latency hides behind the scans (a barrier does not wait for them)
+  int v[RF_BATCH], ev[RF_BATCH];
+  auto load_pass = [&](int p0) {
+#pragma unroll
+    for (int j = 0; j < RF_BATCH; ++j) {
+      const int p = p0 + j * RF_WAVES * kWave + tid;
+      const int q = p < P ? p : 0;     // (P >= 1 here: the loads stay inside the pair list)
+      v[j] = pair_to_sorted[q];
+      ev[j] = pair_expert[q];
     }
-    if (lane == 0) s_eo[e] = carry;        // the expert's total, for the scan below
+  };
+  if (P > 0) load_pass(0);
+  __syncthreads();
+  // start[w][e] = sum of column e above row w.  Wave q owns rows [q rpw, (q+1) rpw) and
+  // lane l experts l, l+64, ...: a row's experts lie in consecutive words (no bank
+  // conflicts).  Pass 1: per-wave column sums; pass 2: exclusive walk down the rows
+  // from the sum of the waves above.
+  const int rpw = (G + RF_WAVES - 1) / RF_WAVES;
+  const int w_lo = wv * rpw, w_hi = min(G, w_lo + rpw);
+  for (int e = lane; e < E; e += kWave) {
+    int sum = 0;
+    for (int w = w_lo; w < w_hi; ++w) sum += s_tab[w * E + e];
+    s_part[wv][e] = sum;
+  }
+  __syncthreads();
+  for (int e = lane; e < E; e += kWave) {
+    int run = 0;
+    for (int q = 0; q < wv; ++q) run += s_part[q][e];
+    for (int w = w_lo; w < w_hi; ++w) {
+      const int c = s_tab[w * E + e];
+      s_tab[w * E + e] = run;
+      run += c;
+    }
+    if (wv == RF_WAVES - 1) s_eo[e] = run;     // the last wave's walk ends at the total
   }
   __syncthreads();
   const int tot = tid < E ? s_eo[tid] : 0;
@@ -623,17 +682,10 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     if (tid == E - 1) gemm_tile_off[E] = toff + tincl;
   }
   __syncthreads();
-  // the scatter, RF_BATCH pairs per thread with all their loads issued up front
-  constexpr int RF_BATCH = 4;
-  const int P = pair_offsets[T];
-  for (int p0 = 0; p0 < P; p0 += RF_BATCH * RF_WAVES * kWave) {
-    int v[RF_BATCH], ev[RF_BATCH];
-#pragma unroll
-    for (int j = 0; j < RF_BATCH; ++j) {
-      const int p = p0 + j * RF_WAVES * kWave + tid;
-      v[j] = p < P ? pair_to_sorted[p] : 0;
-      ev[j] = p < P ? pair_expert[p] : 0;
-    }
+  // the scatter: pair p of workgroup w's token t with rank r in its expert e goes to
+  // expert_offsets[e] + start[w][e] + r
+  for (int p0 = 0; p0 < P; p0 += RF_PASS) {
+    if (p0 > 0) load_pass(p0);
 #pragma unroll
     for (int j = 0; j < RF_BATCH; ++j) {
       const int p = p0 + j * RF_WAVES * kWave + tid;
@@ -665,8 +717,17 @@ int launch_count_rule(const float* logits, int T, int E, int rule, float thresho
 int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, int norm_topk,
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
                 hipStream_t s) {
-  hipLaunchKernelGGL(topk_kernel, dim3((T + TK_WAVES - 1) / TK_WAVES), dim3(TK_WAVES * kWave), 0, s,
-                     logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight);
+  const dim3 grid((T + TK_WAVES - 1) / TK_WAVES), block(TK_WAVES * kWave);
+  switch (topk_slots(E)) {
+    case 1: hipLaunchKernelGGL(topk_kernel<1>, grid, block, 0, s, logits, k, T, E, k_max, norm_topk,
+                               pair_offsets, pair_expert, pair_weight); break;
+    case 2: hipLaunchKernelGGL(topk_kernel<2>, grid, block, 0, s, logits, k, T, E, k_max, norm_topk,
+                               pair_offsets, pair_expert, pair_weight); break;
+    case 3: hipLaunchKernelGGL(topk_kernel<3>, grid, block, 0, s, logits, k, T, E, k_max, norm_topk,
+                               pair_offsets, pair_expert, pair_weight); break;
+    default: hipLaunchKernelGGL(topk_kernel<4>, grid, block, 0, s, logits, k, T, E, k_max, norm_topk,
+                                pair_offsets, pair_expert, pair_weight); break;
+  }
   return launch_status();
 }
 
@@ -683,10 +744,16 @@ int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int 
                        float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
                        int32_t* gemm_tile_off, hipStream_t s) {
-  hipLaunchKernelGGL(route_fused_kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave),
-                     0, s, logits, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight,
-                     pairs_out, done, hist, expert_offsets, sorted_token, pair_to_sorted,
-                     gemm_tile_off);
+  auto kernel = route_fused_kernel<4>;
+  switch (topk_slots(E)) {
+    case 1: kernel = route_fused_kernel<1>; break;
+    case 2: kernel = route_fused_kernel<2>; break;
+    case 3: kernel = route_fused_kernel<3>; break;
+    default: break;
+  }
+  hipLaunchKernelGGL(kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave), 0, s, logits,
+                     k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight, pairs_out, done,
+                     hist, expert_offsets, sorted_token, pair_to_sorted, gemm_tile_off);
   return launch_status();
 }
 
