@@ -91,7 +91,8 @@ bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
     o += align_up(bytes);
     return at;
   };
-  L.logits = take(sizeof(float) * static_cast<size_t>(T) * E);
+  // scores, or on the fused router + budget path their per-slice partials
+  L.logits = take(sizeof(float) * static_cast<size_t>(T) * E * (front_fits(T, d) ? front_slices(d) : 1));
   L.k = take(sizeof(int32_t) * static_cast<size_t>(T));
   L.done = take(sizeof(int32_t));
   L.pair_offsets = take(sizeof(int32_t) * (static_cast<size_t>(T) + 1));
@@ -376,12 +377,22 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   const int32_t* k = a->k_in;
   // small layers: scores and counts in one launch (independent work side by side)
   const bool front = budget && front_fits(T, d);
+  // score source of the route kernel: finished scores, or the front launch's partials
+  const float* scores = logits;
+  int n_parts = 1;
+  const float* part_bias = nullptr;
+  float* scores_out = nullptr;
   if (front) {
     int32_t* kb = a->k_out ? a->k_out : static_cast<int32_t*>(at(L.k));
-    RFX_TRY(launch_front(a->h, a->w_router, a->router_bias, logits, T, d, E, a->block_idx, a->masked,
-                         a->hist_len, a->conf_prev1, a->conf_prev2, a->seq_offsets, a->active_block,
-                         a->B, a->params, kb, s, done));
+    float* parts = static_cast<float*>(at(L.logits));
+    RFX_TRY(launch_front(a->h, a->w_router, parts, T, d, E, a->block_idx, a->masked, a->hist_len,
+                         a->conf_prev1, a->conf_prev2, a->seq_offsets, a->active_block, a->B,
+                         a->params, kb, s, done));
     k = kb;
+    scores = parts;
+    n_parts = front_slices(d);
+    part_bias = a->router_bias;
+    scores_out = a->logits_out;
   } else {
     RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s, done));
   }
@@ -405,7 +416,8 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // at most RF_HIST_MAX (token block, expert) counts the pairs are also sorted there,
   // otherwise by the permutation launches.  Either way the sort writes the GEMM tile
   // plan at the head of gws.
-  RFX_TRY(launch_route_fused(logits, k, T, E, kcap, a->norm_topk, pair_offsets, pair_expert,
+  RFX_TRY(launch_route_fused(scores, n_parts, static_cast<size_t>(T) * E, part_bias, scores_out, k,
+                             T, E, kcap, a->norm_topk, pair_offsets, pair_expert,
                              pair_weight, a->pairs_out, done, static_cast<int32_t*>(at(L.route_hist)),
                              expert_offsets, sorted_token, pair_to_sorted,
                              static_cast<int32_t*>(gws), s));

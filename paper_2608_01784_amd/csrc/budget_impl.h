@@ -62,6 +62,19 @@ __device__ __forceinline__ double rank_key(const BudgetConsts& p, float c1f, flo
   }
 }
 
+// Sum over aligned groups of N lanes (N a power of two up to 16), every lane of a group
+// receiving its group's sum: the symmetric DPP steps of wave_sum_i32 that stay inside
+// the group.
+template <int N>
+__device__ __forceinline__ int lane_group_sum(int v) {
+  uint32_t x = static_cast<uint32_t>(v);
+  if (N >= 2) x += dpp_u32<kDppXor1>(x);
+  if (N >= 4) x += dpp_u32<kDppXor2>(x);
+  if (N >= 8) x += dpp_u32<kDppHalfMirror>(x);
+  if (N >= 16) x += dpp_u32<kDppMirror>(x);
+  return static_cast<int>(x);
+}
+
 template <int NT>
 __device__ __forceinline__ int block_sum(int v, int* red) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -187,24 +200,29 @@ __device__ __forceinline__ void budget_sequence(
         const int cnt = s_off[BG_PER_THREAD * NW];
         __syncthreads();
         if (d0 == c0 && cnt <= kWave) {
-          // the candidates rank themselves: lane x of wave 0 counts the staged
-          // candidates that precede candidate x (key descending, token ascending),
-          // reading each one's key from a register of its lane
-          if (wv == 0) {
-            const double kx = lane < cnt ? s_key[lane] : 0.0;
-            const int ix = lane < cnt ? s_idx[lane] : 0;
-            int before = 0;
-            const long long kbits = __double_as_longlong(kx);
-            for (int y = 0; y < cnt; ++y) {       // y is uniform: scalar reads of lane y
-              const int lo32 = __builtin_amdgcn_readlane(static_cast<int>(kbits & 0xffffffff), y);
-              const int hi32 = __builtin_amdgcn_readlane(static_cast<int>(kbits >> 32), y);
-              const double ky = __longlong_as_double(
-                  (static_cast<long long>(hi32) << 32) | static_cast<unsigned int>(lo32));
-              const int iy = __builtin_amdgcn_readlane(ix, y);
-              before += (ky > kx || (ky == kx && iy < ix)) ? 1 : 0;
+          // the candidates rank themselves: LPX lanes per staged candidate x each count
+          // the candidates among every LPX-th one that precede x (key descending, token
+          // ascending), and a DPP sum over the LPX lanes gives x's rank within the slice
+          constexpr int LPX = BG_THREADS / kWave;
+          static_assert(LPX >= 1 && LPX <= 16 && (LPX & (LPX - 1)) == 0, "lanes per candidate");
+          const int x = tid / LPX, yq = tid % LPX;
+          int before = 0;
+          if (x < cnt) {
+            const double kx = s_key[x];
+            const int ix = s_idx[x];
+#pragma unroll
+            for (int u = 0; u < kWave / LPX; ++u) {
+              const int y = yq + LPX * u;
+              if (y < cnt) {
+                const double ky = s_key[y];
+                const int iy = s_idx[y];
+                before += (ky > kx || (ky == kx && iy < ix)) ? 1 : 0;
+              }
             }
-            if (lane < cnt) s_idx[lane] = before;      // slot -> rank within the slice
           }
+          before = lane_group_sum<LPX>(before);
+          __syncthreads();                              // every read of s_idx done
+          if (x < cnt && yq == 0) s_idx[x] = before;    // slot -> rank within the slice
           __syncthreads();
 #pragma unroll
           for (int r = 0; r < BG_PER_THREAD; ++r)

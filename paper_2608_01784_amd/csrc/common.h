@@ -167,9 +167,13 @@ int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t*
 int launch_fill_i32(int32_t* dst, int32_t value, int n, hipStream_t s);
 
 // Router scores and REFLEX counts in one launch; only for shapes where front_fits().
+// The scores come out as front_slices(d) fp32 partials without the bias, parts[s][T][E]
+// (slice s covers d columns [256 s, 256 s + 256)); a score is the partials added in
+// slice order, plus the bias.
 bool front_fits(int T, int d);
-int launch_front(const uint16_t* h, const float* w, const float* bias, float* logits, int T, int d,
-                 int E, const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
+int front_slices(int d);
+int launch_front(const uint16_t* h, const float* w, float* parts, int T, int d, int E,
+                 const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,
                  const float* c1, const float* c2, const int32_t* seq_offsets,
                  const int32_t* active_block, int B, const reflex_alloc_params& p, int32_t* k_out,
                  hipStream_t s, int32_t* zero_word = nullptr);
@@ -194,9 +198,13 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
 // Pair offsets + TopK, and the permutation too when route_fused_sorts(T, E) and `done`
 // is a device word the preceding launch set to zero (hist: route_hist_bytes(T, E) of
 // scratch); else done must be NULL and launch_permute follows.  pairs_out nullable.
+// The scores are n_parts partials part_stride floats apart, added in order, plus bias
+// (nullable); n_parts = 1 with bias NULL reads finished scores.  logits_out (nullable)
+// receives the finished scores.
 bool route_fused_sorts(int T, int E);
 size_t route_hist_bytes(int T, int E);
-int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
+int launch_route_fused(const float* logits, int n_parts, size_t part_stride, const float* bias,
+                       float* logits_out, const int32_t* k, int T, int E, int k_max,
                        int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
                        float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,

@@ -27,8 +27,13 @@ struct TopkRow {
   float val[NX];
 };
 
+// A score may arrive as n_parts partials part_stride floats apart (the split-K router
+// tiles of the fused router + budget launch): they are added in order, then the bias
+// (nullable).  n_parts = 1 with no bias reads finished scores.
 template <int NX>
-__device__ __forceinline__ TopkRow<NX> topk_load(const float* __restrict__ row, int E) {
+__device__ __forceinline__ TopkRow<NX> topk_load(const float* __restrict__ row, int E,
+                                                 int n_parts = 1, size_t part_stride = 0,
+                                                 const float* __restrict__ bias = nullptr) {
   const int lane = threadIdx.x & 63;
   TopkRow<NX> r;
   // unconditional loads (lanes past E read expert E-1 and discard it), all in flight
@@ -38,6 +43,31 @@ __device__ __forceinline__ TopkRow<NX> topk_load(const float* __restrict__ row, 
   for (int j = 0; j < NX; ++j) {
     const int e = lane + kWave * j;
     v[j] = row[e < E ? e : E - 1];
+  }
+  if (n_parts > 1) {
+    constexpr int PB = 8;     // partials loaded per batch
+    for (int s0 = 1; s0 < n_parts; s0 += PB) {
+      float pv[PB][NX];
+#pragma unroll
+      for (int u = 0; u < PB; ++u)
+#pragma unroll
+        for (int j = 0; j < NX; ++j) {
+          const int e = lane + kWave * j, sp = min(s0 + u, n_parts - 1);
+          pv[u][j] = row[static_cast<size_t>(sp) * part_stride + (e < E ? e : E - 1)];
+        }
+#pragma unroll
+      for (int u = 0; u < PB; ++u)
+#pragma unroll
+        for (int j = 0; j < NX; ++j)
+          if (s0 + u < n_parts) v[j] += pv[u][j];
+    }
+  }
+  if (bias != nullptr) {
+#pragma unroll
+    for (int j = 0; j < NX; ++j) {
+      const int e = lane + kWave * j;
+      v[j] += bias[e < E ? e : E - 1];
+    }
   }
 #pragma unroll
   for (int j = 0; j < NX; ++j) {
@@ -542,7 +572,9 @@ constexpr int RF_HIST_MAX = 16384;       // workgroups x experts held in LDS by 
 
 template <int NX>
 __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
-    const float* __restrict__ logits, const int32_t* __restrict__ k, int T, int E, int k_max,
+    const float* __restrict__ logits, int n_parts, size_t part_stride,
+    const float* __restrict__ bias, float* __restrict__ logits_out,
+    const int32_t* __restrict__ k, int T, int E, int k_max,
     int norm_topk, int32_t* __restrict__ pair_offsets, int32_t* __restrict__ pair_expert,
     float* __restrict__ pair_weight, int32_t* __restrict__ pairs_out, int32_t* __restrict__ done,
     int32_t* __restrict__ hist, int32_t* __restrict__ expert_offsets,
@@ -556,7 +588,13 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   for (int e = tid; e < REFLEX_MAX_EXPERTS; e += RF_WAVES * kWave) s_mask[e] = 0;
   const int i = t0 + wv;
   // this token's scores are loaded first: their latency overlaps the count prefix
-  const TopkRow<NX> row = topk_load<NX>(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E);
+  const TopkRow<NX> row = topk_load<NX>(logits + static_cast<size_t>(i < T ? i : T - 1) * E, E,
+                                        n_parts, part_stride, bias);
+  if (logits_out != nullptr && i < T) {
+#pragma unroll
+    for (int j = 0; j < NX; ++j)
+      if (lane + kWave * j < E) logits_out[static_cast<size_t>(i) * E + lane + kWave * j] = row.val[j];
+  }
   int part = 0;     // (unrolled so that several count loads are in flight at once)
 #pragma unroll 8
   for (int t = tid; t < t0; t += RF_WAVES * kWave) part += clamp_count(k[t], k_max);
@@ -739,7 +777,8 @@ size_t route_hist_bytes(int T, int E) {
   return align_up(static_cast<size_t>((T + RF_WAVES - 1) / RF_WAVES) * E * sizeof(int32_t));
 }
 
-int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int k_max,
+int launch_route_fused(const float* logits, int n_parts, size_t part_stride, const float* bias,
+                       float* logits_out, const int32_t* k, int T, int E, int k_max,
                        int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,
                        float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
@@ -752,7 +791,7 @@ int launch_route_fused(const float* logits, const int32_t* k, int T, int E, int 
     default: break;
   }
   hipLaunchKernelGGL(kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave), 0, s, logits,
-                     k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight, pairs_out, done,
+                     n_parts, part_stride, bias, logits_out, k, T, E, k_max, norm_topk, pair_offsets, pair_expert, pair_weight, pairs_out, done,
                      hist, expert_offsets, sorted_token, pair_to_sorted, gemm_tile_off);
   return launch_status();
 }

@@ -147,5 +147,88 @@ __device__ __forceinline__ void router_tile(int bx, int by, const uint16_t* __re
   }
 }
 
+// ---- split-K partial tiles (the fused router + budget launch) ----
+// The small-T router's cost is bytes through each CU: a workgroup that owns TM tokens
+// x 16 experts over the whole of d moves (2 TM + 4 x 16) d bytes, and the fp32 W_r
+// block is re-read by every token tile.  Here a workgroup owns 32 tokens x 64 experts
+// over one 256-wide slice of d (80 KB: 16 KB of h, 64 KB of W_r) and writes the fp32
+// partial scores of its slice; the consumer adds the d / 256 partials of a score in
+// slice order (and the bias), so the result is deterministic.  16 waves: wave (c, q)
+// takes experts 16c..16c+15 and K [64q, 64q+64) of the slice for both token blocks,
+// loading its own W_r fragments (lane group g holds the 8 contiguous K values 8g..8g+7
+// of each 32-wide step in both operands); the slice's h rows are staged once in LDS by
+// one global_load_lds_dwordx4 copy per wave (two whole 512-byte rows), 16-byte chunk c
+// of row r in slot c ^ (r % 16) so the 16 rows a 16-lane phase reads hit distinct
+// banks.  The four K quarters are summed through LDS in a fixed order.
+constexpr int RS_TM = 32;        // tokens per tile
+constexpr int RS_TE = 64;        // experts per tile
+constexpr int RS_KS = 256;       // K slice per tile (and per partial)
+constexpr int RS_THREADS = 1024;
+
+__device__ __forceinline__ void rs_dma(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+__device__ __forceinline__ void router_split_tile(int bx, int by, int ks,
+                                                  const uint16_t* __restrict__ h,
+                                                  const float* __restrict__ w,
+                                                  float* __restrict__ parts, int T, int d, int E) {
+  __shared__ __attribute__((aligned(16))) uint16_t s_h[RS_TM * RS_KS];
+  __shared__ float s_red[4][RS_TM * RS_TE];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int t0 = bx * RS_TM, e0 = by * RS_TE, k0 = ks * RS_KS;
+  const int c = wv >> 2, q = wv & 3, frow = lane & 15, g = lane >> 4;
+
+  // this wave's W_r fragments: expert e0 + 16c + frow, K k0 + 64q + 32j + 8g .. +7
+  const int e = e0 + 16 * c + frow;
+  const float* wp = w + static_cast<size_t>(e < E ? e : E - 1) * d + k0 + 64 * q + 8 * g;
+  float4 wf[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    wf[j][0] = *reinterpret_cast<const float4*>(wp + 32 * j);
+    wf[j][1] = *reinterpret_cast<const float4*>(wp + 32 * j + 4);
+  }
+  // rows 2 wv, 2 wv + 1 of the h slice (rows past T repeat row T-1; their scores are
+  // not stored): lane L fills slot L % 32 of row 2 wv + L / 32
+  {
+    const int r = 2 * wv + (lane >> 5), chunk = (lane & 31) ^ (r & 15);
+    const int t = min(t0 + r, T - 1);
+    rs_dma(h + static_cast<size_t>(t) * d + k0 + 8 * chunk, s_h + 2 * wv * RS_KS);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0f70);     // vmcnt(0): this wave's copy and loads landed
+  __syncthreads();
+
+  f32x4_t acc[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    bf16x8_t w0, w1, w2;
+    split3x8(wf[j][0], wf[j][1], w0, w1, w2);
+    const int kc = (64 * q + 32 * j) / 8 + g;     // the lane's logical 16-byte chunk
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int r = 16 * b + frow;
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(s_h + r * RS_KS + 8 * (kc ^ (r & 15)));
+      acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w0, acc[b], 0, 0, 0);
+      acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w1, acc[b], 0, 0, 0);
+      acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w2, acc[b], 0, 0, 0);
+    }
+  }
+  // accumulator: lane l, register i -> token row 16 b + 4 (l/16) + i, expert 16 c + l % 16
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      s_red[q][(16 * b + 4 * g + i) * RS_TE + 16 * c + frow] = acc[b][i];
+  __syncthreads();
+  for (int x = tid; x < RS_TM * RS_TE; x += RS_THREADS) {
+    const int t = t0 + x / RS_TE, ee = e0 + x % RS_TE;
+    if (t < T && ee < E)
+      parts[static_cast<size_t>(ks) * T * E + static_cast<size_t>(t) * E + ee] =
+          ((s_red[0][x] + s_red[1][x]) + s_red[2][x]) + s_red[3][x];
+  }
+}
+
 }  // namespace
 }  // namespace rfx

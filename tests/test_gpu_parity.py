@@ -435,6 +435,10 @@ def compare_layer(name, out, k, logits, norm_topk=1, tag=""):
     # (ii) independent: the oracle's own fp64 logits; tokens whose selected set differs
     # must be explained by a logit margin below the router tolerance
     r_or = oracle.router_scores(w.h, hw["w_router"], w.router_bias)
+    # the forward's own scores (split-K partials added by the route kernel on the fused
+    # router + budget path) within the router tolerance of the fp64 scores, per row
+    err = np.abs(logits - r_or).max(axis=1)
+    assert np.all(err <= 1e-4 * np.abs(r_or).max(axis=1)), float((err / np.abs(r_or).max(axis=1)).max())
     route_i = oracle.topk_route(r_or, k, norm_topk)
     ref_i = oracle.moe_layer(w.h, route_i, weights_of(name), w.E, shared=hw["shared"], tokens=toks)
     tl = np.arange(w.T) if toks is None else toks
