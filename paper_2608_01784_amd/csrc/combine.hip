@@ -28,6 +28,17 @@ __global__ __launch_bounds__(256) void combine_kernel(
   p0 = p0 < 0 ? 0 : (p0 > cap ? cap : p0);
   p1 = p1 < p0 ? p0 : (p1 > cap ? cap : p1);
   const size_t tok_off = static_cast<size_t>(i) * d;
+  // the token's pair rows and weights, lane j of every wave holding pair p0 + j (one
+  // vector load each instead of a scalar load per pair ahead of its row load); a
+  // forward's count is at most REFLEX_MAX_K <= 64
+  const int lane = threadIdx.x & 63, np = p1 - p0;
+  int prow = 0;
+  float pw = 0.0f;
+  if (lane < np) {
+    prow = pair_to_sorted[p0 + lane];
+    prow = prow < 0 ? 0 : (prow >= cap ? cap - 1 : prow);
+    pw = pair_weight[p0 + lane];
+  }
   for (int v = threadIdx.x * 8; v < d; v += 256 * 8) {
     // the token's own rows (shared expert, residuals) are loaded first, so they are in
     // flight with the expert rows; they are still added after them, in the same order
@@ -36,12 +47,26 @@ __global__ __launch_bounds__(256) void combine_kernel(
     const uint4 av = res_a ? *reinterpret_cast<const uint4*>(res_a + tok_off + v) : zero;
     const uint4 bv = res_b ? *reinterpret_cast<const uint4*>(res_b + tok_off + v) : zero;
     float acc[8] = {};
-#pragma unroll 4
-    for (int p = p0; p < p1; ++p) {       // (unrolled: several rows in flight at once)
-      int row = pair_to_sorted[p];
-      row = row < 0 ? 0 : (row >= cap ? cap - 1 : row);
-      add_bf16x8(acc, *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v),
-                 pair_weight[p]);
+    constexpr int CB = 16;     // expert rows in flight per batch
+    if (np > kWave) {          // (more pairs than lanes: only through reflex_combine)
+      for (int p = p0; p < p1; ++p) {
+        int row = pair_to_sorted[p];
+        row = row < 0 ? 0 : (row >= cap ? cap - 1 : row);
+        add_bf16x8(acc, *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v),
+                   pair_weight[p]);
+      }
+    }
+    for (int q = 0; q < (np > kWave ? 0 : np); q += CB) {
+      uint4 r[CB];
+#pragma unroll
+      for (int u = 0; u < CB; ++u) {     // past the count: the last row again, not added
+        const int row = __builtin_amdgcn_readlane(prow, min(q + u, np - 1));
+        r[u] = *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v);
+      }
+#pragma unroll
+      for (int u = 0; u < CB; ++u)
+        if (q + u < np)
+          add_bf16x8(acc, r[u], __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pw), q + u)));
     }
     if (shared_y) add_bf16x8(acc, sv, 1.0f);
     if (res_a) add_bf16x8(acc, av, 1.0f);
