@@ -343,7 +343,7 @@ typedef struct {
   uint16_t *out;                             /* [T, d] bf16                              */
   int32_t  *k_out;                           /* [T] counts used, or NULL                 */
   int32_t  *pairs_out;                       /* [1] P, or NULL                           */
-  float    *logits_out;                      /* [T, E] router scores, or NULL            */
+  float    *logits_out;                      /* [T, E] router scores (bias added), or NULL */
 } reflex_moe_args;
 
 /* ws: >= reflex_workspace_size(T, E, d, f, f_shared, kcap) bytes, 256-byte aligned. */
@@ -352,8 +352,9 @@ int reflex_moe_forward(const reflex_moe_args* args, void* ws, size_t ws_bytes, v
 /*
  * reflex_moe_forward with timing marks, for benchmarks: identical work, plus
  * hipEventRecord(stage_events[i], stream) at each stage boundary:
- *   0 start, 1 router done (for layers with T < 4096 the REFLEX counts are
- *   computed in the same launch), 2 counts done (budget / rule / uniform fill / reuse),
+ *   0 start, 1 router done (for layers with T < 4096 on the REFLEX budget path one
+ *   launch computes the counts and the scores as d/256 partial sums, which step 3 adds
+ *   with the bias), 2 counts done (budget / rule / uniform fill / reuse),
  *   3 count scan + TopK done, 4 permutation + GEMM tile plan done,
  *   5 gate/up GEMM done, 6 down GEMM done, 7 shared expert done, 8 combine done.
  * stage_events: host array of REFLEX_N_STAGE_EVENTS hipEvent_t handles created by
