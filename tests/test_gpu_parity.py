@@ -654,3 +654,27 @@ def test_fused_consecutive_calls_and_no_pairs(torch):
             continue
         ref = _fuzz_ref(w, lay.logits.cpu().numpy().astype(np.float64), k)
         layer_tolerance_check(out, ref, f"consecutive call {n}")
+
+
+@pytest.mark.parametrize("seed,T,d,E", [(130, 333, 1024, 100), (134, 95, 512, 256), (132, 1000, 768, 64)])
+def test_fused_split_router_partials(torch, seed, T, d, E):
+    # on the fused router + budget path the scores come out as d/256 partial sums that
+    # the route kernel adds in slice order, with the bias: several slices (3 of them
+    # for d = 768), expert blocks past 64 with E off a multiple of 64, token counts off
+    # the 32-token tile, several sequences, a router bias
+    import dataclasses
+    w = make_fuzz_workload(seed, T=T, d=d, E=E, f=128, k_max=min(E, 8))
+    if w.router_bias is None:
+        bias = (np.random.default_rng(seed).standard_normal(E) * 0.5).astype(np.float32)
+        w = dataclasses.replace(w, router_bias=bias)
+    assert len(w.seq_offsets) > 2
+    lay, st = _fuzz_layer(torch, w)
+    out = oracle.bf16_to_f64(bf16_bits(lay.forward(to_device(w.h), st)))
+    torch.cuda.synchronize()
+    k = lay.k.cpu().numpy()
+    assert np.array_equal(k, oracle_budget(w).k)
+    logits = lay.logits.cpu().numpy().astype(np.float64)
+    r_or = oracle.router_scores(w.h, w.w_router(), w.router_bias)
+    err = np.abs(logits - r_or).max(axis=1)
+    assert np.all(err <= 1e-4 * np.abs(r_or).max(axis=1)), float((err / np.abs(r_or).max(axis=1)).max())
+    layer_tolerance_check(out, _fuzz_ref(w, logits, k), f"split router T={T} d={d} E={E}")
