@@ -1,6 +1,7 @@
 // C ABI of libreflex: host-side validation, workspace carving and launch order.
 // Every check happens before the first launch; nothing here allocates, frees or
 // synchronises.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -91,8 +92,9 @@ bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
     o += align_up(bytes);
     return at;
   };
-  // scores, or on the fused router + budget path their per-slice partials
-  L.logits = take(sizeof(float) * static_cast<size_t>(T) * E * (front_fits(T, d) ? front_slices(d) : 1));
+  // scores, or on the split-K router paths their per-slice partials
+  const int parts = std::max(front_fits(T, d) ? front_slices(d) : 1, router_slices(T, d, E));
+  L.logits = take(sizeof(float) * static_cast<size_t>(T) * E * parts);
   L.k = take(sizeof(int32_t) * static_cast<size_t>(T));
   L.done = take(sizeof(int32_t));
   L.pair_offsets = take(sizeof(int32_t) * (static_cast<size_t>(T) + 1));
@@ -394,7 +396,18 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     part_bias = a->router_bias;
     scores_out = a->logits_out;
   } else {
-    RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s, done));
+    // partial scores for the route kernel to add, unless a count rule reads the scores
+    const int ns = by_rule ? 1 : router_slices(T, d, E);
+    if (ns > 1) {
+      float* parts = static_cast<float*>(at(L.logits));
+      RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, parts, T, d, E, s, done, ns));
+      scores = parts;
+      n_parts = ns;
+      part_bias = a->router_bias;
+      scores_out = a->logits_out;
+    } else {
+      RFX_TRY(launch_router(a->h, a->w_router, a->router_bias, logits, T, d, E, s, done));
+    }
   }
   RFX_TRY(mark(1));
   if (k == nullptr) {

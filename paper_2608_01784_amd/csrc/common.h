@@ -154,9 +154,13 @@ RFX_DEVICE int clamp_count(int k, int k_max) { return k < 0 ? 0 : (k > k_max ? k
 namespace rfx {
 
 // zero_word (nullable): set to 0 by the launch (the counter the fused route kernel that
-// follows in the same forward expects to find at zero).
+// follows in the same forward expects to find at zero).  n_slices > 1 (only a value of
+// router_slices(T, d, E)): logits receives n_slices fp32 partial score arrays [T, E]
+// without the bias, slice s covering d columns [s d/n, (s+1) d/n); a score is the
+// partials added in slice order, plus the bias.
+int router_slices(int T, int d, int E);
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
-                  int d, int E, hipStream_t s, int32_t* zero_word = nullptr);
+                  int d, int E, hipStream_t s, int32_t* zero_word = nullptr, int n_slices = 1);
 
 // pairs_out may be NULL (the fused forward takes P from the count scan instead).
 int launch_budget(const int32_t* block_idx, const uint8_t* masked, const int8_t* hist_len,

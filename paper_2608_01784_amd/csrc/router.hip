@@ -60,7 +60,10 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
                                                                 const float* __restrict__ bias,
                                                                 float* __restrict__ logits, int T,
                                                                 int d, int E,
-                                                                int32_t* __restrict__ zero_word) {
+                                                                int32_t* __restrict__ zero_word,
+                                                                int n_slices) {
+  // n_slices > 1: this workgroup covers d columns [ks kd, ks kd + kd), kd = d / n_slices,
+  // ks = blockIdx.z, and writes the partial scores (no bias) to logits + ks T E
   constexpr int TB = TM / 16;                          // token blocks per wave
   constexpr int H_ELEMS = TM * RB_BK;                  // bf16 per h slice
   constexpr int W_ELEMS = RB_TE * RB_BK;               // fp32 per W slice
@@ -72,8 +75,10 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int t0 = blockIdx.x * TM, e0 = blockIdx.y * RB_TE;
-  const int nk = d / RB_BK;
-  if (zero_word != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) *zero_word = 0;
+  const int kd = d / n_slices, kbase = blockIdx.z * kd;
+  const int nk = kd / RB_BK;
+  if (zero_word != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && tid == 0)
+    *zero_word = 0;
 
   // copy sources: lane L of an h op fills row 8q + L/8, slot L%8; of a W op row 4q + L/16,
   // slot L%16; rows past T or E repeat the last valid row (their results are not stored)
@@ -84,14 +89,14 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
     const int q = wv * H_OPS + j, r = 8 * q + lane / 8;
     const int c = (lane % 8) ^ ((r / 2) % 8);
     const int t = min(t0 + r, T - 1);
-    hp[j] = h + static_cast<size_t>(t) * d + c * 8;
+    hp[j] = h + static_cast<size_t>(t) * d + kbase + c * 8;
   }
 #pragma unroll
   for (int j = 0; j < W_OPS; ++j) {
     const int q = wv * W_OPS + j, r = 4 * q + lane / 16;
     const int c = (lane % 16) ^ (r % 16);
     const int e = min(e0 + r, E - 1);
-    wp[j] = w + static_cast<size_t>(e) * d + c * 4;
+    wp[j] = w + static_cast<size_t>(e) * d + kbase + c * 4;
   }
   auto issue = [&](int kt) {
     const int buf = kt % S, k0 = kt * RB_BK;
@@ -138,40 +143,60 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
   // accumulator: lane l, register r -> token row 4 (l/16) + r, expert column l % 16
   const int e = e0 + 16 * wv + (lane & 15);
   if (e < E) {
-    const float be = bias ? bias[e] : 0.0f;
+    const float be = (bias && n_slices == 1) ? bias[e] : 0.0f;
+    float* out = logits + static_cast<size_t>(blockIdx.z) * T * E;
 #pragma unroll
     for (int b = 0; b < TB; ++b)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = t0 + 16 * b + 4 * (lane >> 4) + r;
-        if (t < T) logits[static_cast<size_t>(t) * E + e] = acc[b][r] + be;
+        if (t < T) out[static_cast<size_t>(t) * E + e] = acc[b][r] + be;
       }
   }
 }
 
 }  // namespace
 
+// K slices of the split-K router for T >= 4096 (1: finished scores).  The 128-token x
+// 64-expert LDS-staged tiles re-read neither operand much (h once per 64 experts, W_r
+// once per 128 tokens), so where they are too few to fill the GPU the K range is split
+// instead of shrinking the tiles: up to ~512 workgroups (two fit a CU), slices of at
+// least 256 columns.
+int router_slices(int T, int d, int E) {
+  if (T < 4096 || d % RB_BK != 0) return 1;
+  const long tiles = static_cast<long>((T + 127) / 128) * ((E + RB_TE - 1) / RB_TE);
+  int ns = 1;
+  while (tiles * ns * 2 <= 512 && d % (2 * ns * 256) == 0) ns *= 2;
+  return ns;
+}
+
 int launch_router(const uint16_t* h, const float* w, const float* bias, float* logits, int T,
-                  int d, int E, hipStream_t s, int32_t* zero_word) {
+                  int d, int E, hipStream_t s, int32_t* zero_word, int n_slices) {
   // A workgroup's loads all pass through one CU, so tiles are sized to spread the
-  // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves.  The
-  // LDS-staged kernel runs its 64-wide K steps one after another, so its tiles are made
-  // small enough for its grid to fill the GPU: 128 x 64 tiles where that gives 512 or
-  // more (T = 16384, E = 256: half the time of the register kernel), else 32 x 64 tiles
-  // (T = 4096, E = 256: 33 us against 39 us for 64 x 64 register tiles).  With at most
-  // 64 experts (one expert block) the register kernel with 32-token tiles and K split
-  // over 8 waves is faster still (T = 8192, E = 64: 29 us against 34 us and 38 us for
-  // the LDS kernel and 64 x 64 register tiles; all measured).
+  // traffic over many CUs: small T uses 16 x 16 tiles with K split over 16 waves.  For
+  // T >= 4096 the split-K path (n_slices > 1, partial scores for the caller to add) runs
+  // 128 x 64 tiles over a slice of d each.  With finished scores requested: 128 x 64
+  // tiles where that gives 512 or more (T = 16384, E = 256), else 32 x 64 tiles (T = 4096,
+  // E = 256: 33 us against 39 us for 64 x 64 register tiles), and with at most 64 experts
+  // the register kernel with 32-token tiles and K split over 8 waves (T = 8192, E = 64:
+  // 29 us against 34 us and 38 us for the LDS kernel and 64 x 64 register tiles; all
+  // measured).
+  if (n_slices > 1) {
+    hipLaunchKernelGGL((router_big_kernel<128, 2>),
+                       dim3((T + 127) / 128, (E + RB_TE - 1) / RB_TE, n_slices), dim3(RB_THREADS), 0,
+                       s, h, w, bias, logits, T, d, E, zero_word, n_slices);
+    return launch_status();
+  }
   const long big_tiles = static_cast<long>((T + 127) / 128) * ((E + RB_TE - 1) / RB_TE);
   if (big_tiles >= 512) {
     hipLaunchKernelGGL((router_big_kernel<128, 2>), dim3((T + 127) / 128, (E + RB_TE - 1) / RB_TE),
-                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word);
+                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word, 1);
   } else if (T >= 4096 && E <= 64 && d % (RT_TK * 8) == 0) {
     hipLaunchKernelGGL((router_mfma_kernel<32, 4, 8, 2>), dim3((T + 31) / 32, (E + 63) / 64),
                        dim3(512), 0, s, h, w, bias, logits, T, d, E, zero_word);
   } else if (T >= 4096) {
     hipLaunchKernelGGL((router_big_kernel<32, 2>), dim3((T + 31) / 32, (E + RB_TE - 1) / RB_TE),
-                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word);
+                       dim3(RB_THREADS), 0, s, h, w, bias, logits, T, d, E, zero_word, 1);
   } else if (d % (RT_TK * 16) == 0) {
     hipLaunchKernelGGL((router_mfma_kernel<16, 1, 16, 4>), dim3((T + 15) / 16, (E + 15) / 16),
                        dim3(1024), 0, s, h, w, bias, logits, T, d, E, zero_word);
