@@ -6,6 +6,7 @@
 #include <cstring>
 
 #include <initializer_list>
+#include <mutex>
 
 #include "common.h"
 
@@ -74,6 +75,35 @@ int check_rule(int rule, float threshold) {
     return threshold >= 0.0f && threshold < 1.0f ? REFLEX_OK : REFLEX_ERR_PARAM;
   return REFLEX_ERR_PARAM;
 }
+
+// A second stream per device for work of the forward that reads nothing the routing
+// computes (the shared expert): non-blocking (no implicit ordering with the legacy
+// default stream), default priority, created on first use and kept for the life of the
+// process.  NULL if it cannot be created (the work then stays on the caller's stream).
+hipStream_t side_stream() {
+  static std::mutex mu;
+  static hipStream_t streams[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> g(mu);
+  if (streams[dev] == nullptr) {
+    hipStream_t st = nullptr;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    streams[dev] = st;
+  }
+  return streams[dev];
+}
+
+// The fork and join events of one forward, created per call (so concurrent callers never
+// share one) and released at scope exit; a destroyed event's pending record and waits
+// still complete.
+struct ForkJoin {
+  hipEvent_t fork = nullptr, join = nullptr;
+  ~ForkJoin() {
+    if (fork) (void)hipEventDestroy(fork);
+    if (join) (void)hipEventDestroy(join);
+  }
+};
 
 struct Layout {
   size_t logits, k, done, pair_offsets, pair_expert, pair_weight, expert_offsets, sorted_token,
@@ -376,6 +406,24 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // the fused route kernel's completion counter, zeroed by the router launch
   int32_t* done = route_fused_sorts(T, E) ? static_cast<int32_t*>(at(L.done)) : nullptr;
   RFX_TRY(mark(0));
+  // The shared expert reads only h: on the side stream it runs beside the routing
+  // launches, which leave most CUs idle, and joins the caller's stream before the combine.
+  // The stage-timed variant keeps it in line, so that its stage time is its own.
+  uint16_t* shared_y_buf = fs ? static_cast<uint16_t*>(at(L.shared_y)) : nullptr;
+  ForkJoin fj;
+  bool shared_forked = false;
+  if (fs && ev == nullptr) {
+    hipStream_t side = side_stream();
+    if (side != nullptr && hipEventCreateWithFlags(&fj.fork, hipEventDisableTiming) == hipSuccess &&
+        hipEventCreateWithFlags(&fj.join, hipEventDisableTiming) == hipSuccess) {
+      if (hipEventRecord(fj.fork, s) != hipSuccess || hipStreamWaitEvent(side, fj.fork, 0) != hipSuccess)
+        return REFLEX_ERR_LAUNCH;
+      RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, shared_y_buf,
+                                  at(L.shared_act), side));
+      if (hipEventRecord(fj.join, side) != hipSuccess) return REFLEX_ERR_LAUNCH;
+      shared_forked = true;
+    }
+  }
   const int32_t* k = a->k_in;
   // small layers: scores and counts in one launch (independent work side by side)
   const bool front = budget && front_fits(T, d);
@@ -445,8 +493,11 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, a->w_down_packed, E, d, f, cap, y, gws, s));
   RFX_TRY(mark(6));
   const uint16_t* shared_y = nullptr;
-  if (fs) {
-    uint16_t* sy = static_cast<uint16_t*>(at(L.shared_y));
+  if (fs && shared_forked) {
+    if (hipStreamWaitEvent(s, fj.join, 0) != hipSuccess) return REFLEX_ERR_LAUNCH;
+    shared_y = shared_y_buf;
+  } else if (fs) {
+    uint16_t* sy = shared_y_buf;
     RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, sy,
                                 at(L.shared_act), s));
     shared_y = sy;
