@@ -373,7 +373,8 @@ def test_grouped_swiglu(torch, name):
 @pytest.mark.parametrize("with_shared", [False, True])
 @pytest.mark.parametrize("T,d,E,kmax", [(1, 128, 4, 2), (333, 256, 16, 6), (1024, 2048, 64, 12),
                                         (64, 256, 32, 32),     # up to 32 pairs: two batches of rows
-                                        (40, 256, 96, 80)])    # > 64 pairs: the per-pair loop
+                                        (40, 256, 96, 80),     # > 64 pairs: the per-pair loop
+                                        (4100, 256, 32, 20)])  # T >= 4096: batches of 8 rows
 def test_combine(torch, T, d, E, kmax, with_shared):
     L = _lib()
     rng = np.random.default_rng(T)
