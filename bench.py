@@ -168,16 +168,23 @@ def _counter_rows(path):
     return [t[1:] for t in rows]
 
 
-def _per_dispatch_kib(path, counter, kernel=None, stride=1):
-    """Mean counter value (KiB) per dispatch of `kernel` (every `stride`-th of its
-    dispatches from the first); without a kernel name, of the dispatches with the largest
-    reading (the calibration copy)."""
+def _per_dispatch_kib(path, counter, kernel=None, per_forward=1):
+    """Mean counter value (KiB) per dispatch of `kernel`; without a kernel name, of the
+    dispatches with the largest reading (the calibration copy).  With `per_forward` = 2
+    each forward launches the kernel twice (routed experts and the shared expert, on two
+    streams, so either may come first): the dispatches are taken in consecutive pairs and
+    the larger reading of each pair is the routed launch (it reads and writes P > T rows
+    against the shared expert's T, and all the routed weights)."""
     vals = [(n, v) for n, c, v in _counter_rows(path) if c == counter]
     if kernel is None:
         top = max(v for _, v in vals)
         sel = [v for _, v in vals if v >= 0.5 * top]
     else:
-        sel = [v for n, v in vals if n == kernel][::stride]
+        mine = [v for n, v in vals if n == kernel]
+        if len(mine) % per_forward:
+            raise SystemExit(f"{len(mine)} {counter} dispatches of {kernel} in {path}: "
+                             f"not {per_forward} per forward")
+        sel = [max(mine[i:i + per_forward]) for i in range(0, len(mine), per_forward)]
     if not sel:
         raise SystemExit(f"no {counter} dispatches of {kernel or 'the copy'} in {path}")
     return sum(sel) / len(sel), len(sel)
@@ -188,8 +195,8 @@ def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_writ
     """Turn two rocprofv3 --pmc runs of the bench (FETCH_SIZE, WRITE_SIZE) and the same two
     counters on a plain copy of COPY_CAL_BYTES into HBM bytes per GEMM launch, stored in
     the traffic file under the current GEMM source digest.  With a shared expert
-    (`shared`), every forward launches each GEMM kernel twice, routed experts first and
-    the shared expert's dense GEMM after; only the routed launches are counted."""
+    (`shared`), every forward launches each GEMM kernel twice, for the routed experts and
+    for the shared expert's dense GEMM; only the routed launches are counted."""
     cf, _ = _per_dispatch_kib(copy_fetch_csv, "FETCH_SIZE")
     cw, _ = _per_dispatch_kib(copy_write_csv, "WRITE_SIZE")
     k_fetch = COPY_CAL_BYTES / (cf * 1024.0)      # true read bytes per counted byte
@@ -205,9 +212,9 @@ def ingest_pmc(workload, layout, fetch_csv, write_csv, copy_fetch_csv, copy_writ
     for stage, knames in STAGE_KERNELS.items():
         present = {n for n, c, _ in _counter_rows(fetch_csv) if c == "FETCH_SIZE"}
         kname = next((k for k in knames if k in present), knames[0])
-        stride = 2 if shared and kname in STAGE_KERNELS[stage][:1] else 1
-        fk, nf = _per_dispatch_kib(fetch_csv, "FETCH_SIZE", kname, stride)
-        wk, nw = _per_dispatch_kib(write_csv, "WRITE_SIZE", kname, stride)
+        per_fwd = 2 if shared and kname in STAGE_KERNELS[stage][:1] else 1
+        fk, nf = _per_dispatch_kib(fetch_csv, "FETCH_SIZE", kname, per_fwd)
+        wk, nw = _per_dispatch_kib(write_csv, "WRITE_SIZE", kname, per_fwd)
         ent = {"workload": workload, "expert_weights": layout, "kernel": stage,
                "kernel_name": kname, "source_sha256": digest,
                "fetch_kib_per_dispatch": round(fk, 1), "write_kib_per_dispatch": round(wk, 1),
