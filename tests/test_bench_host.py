@@ -61,14 +61,18 @@ def test_ingest_pmc_scales_by_copy_calibration(tmp_path, monkeypatch, tall):
 
 
 def test_ingest_pmc_counts_routed_launches_only_with_a_shared_expert(tmp_path, monkeypatch):
-    # per forward: routed up, routed down, then the shared expert's dense up and down on
-    # the same kernels; only the routed launches (every other one, from the first) count
+    # per forward: the routed up and down GEMMs and the shared expert's dense up and down
+    # on the same kernels, the shared ones on a second stream, so either pair member may
+    # come first; only the routed launch (the larger reading of each pair) counts
     up = "void rfx::(anonymous namespace)::swiglu_gemm_kernel<true>(int)"
     dn = "void rfx::(anonymous namespace)::swiglu_gemm_kernel<false>(int)"
     fetch, write = tmp_path / "f.csv", tmp_path / "w.csv"
     frows, wrows = [], []
-    for _ in range(3):
-        for name, f, w in [(up, 1000, 10), (dn, 500, 50), (up, 7, 1), (dn, 3, 2)]:
+    routed = [(up, 1000, 10), (dn, 500, 50)]
+    shared = [(up, 7, 1), (dn, 3, 2)]
+    for fwd in range(3):
+        order = routed + shared if fwd != 1 else [shared[0], routed[0], shared[1], routed[1]]
+        for name, f, w in order:
             frows.append((name, "FETCH_SIZE", f))
             wrows.append((name, "WRITE_SIZE", w))
     def dump(path, rows):
@@ -92,7 +96,14 @@ def test_ingest_pmc_counts_routed_launches_only_with_a_shared_expert(tmp_path, m
     ent = {e["kernel"]: e for e in json.loads(tf.read_text())["entries"]}
     assert ent["gemm_up"]["dispatches"] == [3, 3]
     assert ent["gemm_up"]["read_bytes"] == 1000 * 1024
+    assert ent["gemm_up"]["write_bytes"] == 10 * 1024
+    assert ent["gemm_down"]["read_bytes"] == 500 * 1024
     assert ent["gemm_down"]["write_bytes"] == 50 * 1024
+    # a launch count that is not two per forward is an error, not a silent mean
+    dump(fetch, frows[:-1])
+    dump(write, wrows[:-1])
+    with pytest.raises(SystemExit):
+        bench.ingest_pmc("wl", "row-major", str(fetch), str(write), str(cf), str(cw), shared=True)
 
 
 def test_ingest_pmc_missing_kernel_is_an_error(tmp_path, monkeypatch):
