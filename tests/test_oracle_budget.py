@@ -247,3 +247,43 @@ def test_signal_variants_rank_by_their_key():
     assert k.tolist() == [10, 14, 12, 14, 12, 12, 12, 10]      # highest c^{t-1} get +2
     k = oracle.assign_budget(b, m, hist, c1, c2, so, act, p.replace(signal=4)).k
     assert k.tolist() == [14, 10, 12, 10, 12, 12, 12, 14]      # lowest c^{t-1} get +2
+
+
+def test_frontier_only_and_progress_only_rank_by_their_own_factor():
+    """Appendix C's single-signal rankings: Frontier Only orders J by F of Eq. (6),
+    Progress Only by P of Eq. (7).  The eight tokens decouple the two factors: F
+    depends only on the forecast c_hat and, being sigma(w/2 + x) sigma(w/2 - x) over
+    tau with x = c_hat - (theta - w/2), falls strictly with |x|; P depends only on the
+    clipped velocity v_bar and falls strictly with it.  Every c is a multiple of 1/32
+    (exact in fp32, and c1 - c2, c1 + v_bar exact in fp64) and no velocity reaches the
+    w/2 clip, so v_bar = c1 - c2 and c_hat = c1 + v_bar."""
+    #           t0     t1      t2     t3      t4       t5       t6       t7
+    c_hat = [0.75, 0.6875, 0.25, 0.5, 0.875, 0.59375, 0.375, 0.71875]
+    v_bar = [0.125, 0.0625, -0.125, -0.0625, 0.09375, 0.0, -0.09375, 0.03125]
+    c1 = np.array([c - v for c, v in zip(c_hat, v_bar)], np.float32)
+    c2 = np.array([a - v for a, v in zip(c1.tolist(), v_bar)], np.float32)
+    hist = np.full(8, 2, np.int8)
+    b = np.ones(8, np.int32)
+    so = np.array([0, 8], np.int32)
+    act = np.array([1], np.int32)
+    m = np.ones(8, np.uint8)
+    # K_cur = 12, delta_cur = 2, q = 0.25 -> outer groups of 2, clamp [1, 16] inactive
+    p = AllocParams.make(8, 4, 2, 1, 16, q=0.25, w_cf=0.30)
+    # by |c_hat - 0.75|: t0 < t7 < t1 < t4 < t5 < t3 < t6 < t2
+    k_f = oracle.assign_budget(b, m, hist, c1, c2, so, act, p.replace(signal=1)).k
+    assert k_f.tolist() == [14, 12, 10, 12, 12, 12, 10, 14]
+    # by v_bar ascending (larger P first): t2 < t6 < t3 < t5 < t7 < t1 < t4 < t0
+    k_p = oracle.assign_budget(b, m, hist, c1, c2, so, act, p.replace(signal=2)).k
+    assert k_p.tolist() == [10, 12, 14, 12, 10, 12, 14, 12]
+    # the keys themselves at t0 (c_hat at the frontier centre, v_bar = 1/8) and t2,
+    # against the logistic evaluated here in tanh form on the fp32 hyper-parameters
+    th, w, tau, vr = f32(0.9), f32(0.30), f32(0.05), f32(0.01)
+    for t in (0, 2):
+        F = logistic((c_hat[t] - th + w) / tau) * logistic((th - c_hat[t]) / tau)
+        P = logistic((vr - v_bar[t]) / tau)
+        kf = oracle.ranking_key(1, c1[t:t + 1], c2[t:t + 1], hist[t:t + 1], th, w, vr, tau)[0]
+        kp = oracle.ranking_key(2, c1[t:t + 1], c2[t:t + 1], hist[t:t + 1], th, w, vr, tau)[0]
+        assert kf == pytest.approx(F, rel=1e-12) and kp == pytest.approx(P, rel=1e-12)
+    # t0 sits at the frontier centre: F = sigma(w / 2 tau)^2 = sigma(3)^2 (w = 0.30)
+    k0 = oracle.ranking_key(1, c1[:1], c2[:1], hist[:1], th, w, vr, tau)[0]
+    assert k0 == pytest.approx(0.9073974670915, abs=2e-7)

@@ -52,6 +52,12 @@ MUTANTS = [
     ("history not shifted", "c2[was_masked] = c1[was_masked]", "c2[was_masked] = c2[was_masked]"),
     ("block advances with tokens left", "if left_in_active == 0 and a[s] < last_block:",
      "if a[s] < last_block:"),
+    ("frontier and progress keys swapped", "SIGNAL_FRONTIER: F, SIGNAL_PROGRESS: P",
+     "SIGNAL_FRONTIER: P, SIGNAL_PROGRESS: F"),
+    ("frontier key ranks by the score", "SIGNAL_FRONTIER: F, SIGNAL_PROGRESS: P",
+     "SIGNAL_FRONTIER: S, SIGNAL_PROGRESS: P"),
+    ("progress key ranks by the score", "SIGNAL_FRONTIER: F, SIGNAL_PROGRESS: P",
+     "SIGNAL_FRONTIER: F, SIGNAL_PROGRESS: S"),
     ("progress guard ties to higher position", "best = J[np.lexsort((J, -ct[J].astype(np.float64)))[0]]",
      "best = J[np.lexsort((-J, -ct[J].astype(np.float64)))[0]]"),
 ]
