@@ -32,7 +32,7 @@ sys.path.insert(0, ROOT)
 METRIC = "MoE-layer tokens/s + TFLOP/s (alloc. expert FLOPs) as % bf16 MFMA peak, var-K"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
-DEFAULT_WORKLOAD = "lladamoe_t1024_e64"
+DEFAULT_WORKLOAD = "lladamoe_stack16_t8192"   # the largest single-GPU workload
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 COPY_CAL_BYTES = 1 << 28       # the plain device copy that calibrates the byte counters
 # rocprofv3 kernel names of the stages with a counter-derived traffic figure
@@ -109,14 +109,22 @@ def expert_counts(lay, h, state, torch):
 
 
 def stage_roofline(stage, ms, d, f, P, touched, T, E):
-    """Algorithmic work of one launch of a stage: bytes each operand must move once,
-    FLOPs of its contraction; bound = the larger of the two times at peak."""
+    """Algorithmic work of one launch of a stage: the bytes the operation itself must
+    move once and the FLOPs of its contraction; bound = the larger of the two times at
+    peak.  For the expert GEMMs the algorithmic bytes are the touched experts' weights
+    plus the layer's input h read once (up) or its output written once (down); the
+    pipeline's own traffic between the stages (the P gathered input rows beyond h, the
+    P activation rows written and read back, the P expert-output rows) is reported as
+    `overhead_bytes` and not credited."""
+    overhead = 0
     if stage == "gemm_up":
         flops = 4 * d * f * P
-        nbytes = touched * 2 * f * d * 2 + P * d * 2 + P * f * 2
+        nbytes = touched * 2 * f * d * 2 + T * d * 2
+        overhead = max(P - T, 0) * d * 2 + P * f * 2
     elif stage == "gemm_down":
         flops = 2 * d * f * P
-        nbytes = touched * d * f * 2 + P * f * 2 + P * d * 2
+        nbytes = touched * d * f * 2 + T * d * 2
+        overhead = P * f * 2 + max(P - T, 0) * d * 2
     elif stage == "router":
         flops = 2 * T * E * d
         nbytes = T * d * 2 + E * d * 4 + T * E * 4
@@ -137,11 +145,13 @@ def stage_roofline(stage, ms, d, f, P, touched, T, E):
         ach = flops / (ms * 1e-3) / 1e12
         return {"kernel": stage, "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "algorithmic_flops": int(flops), "algorithmic_bytes": int(nbytes), "ms": round(ms, 5)}
+                "algorithmic_flops": int(flops), "algorithmic_bytes": int(nbytes),
+                "overhead_bytes": int(overhead), "ms": round(ms, 5)}
     ach = nbytes / (ms * 1e-3) / 1e9
     return {"kernel": stage, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
-            "algorithmic_bytes": int(nbytes), "algorithmic_flops": int(flops), "ms": round(ms, 5)}
+            "algorithmic_bytes": int(nbytes), "algorithmic_flops": int(flops),
+            "overhead_bytes": int(overhead), "ms": round(ms, 5)}
 
 
 def kernel_source_digest() -> str:
@@ -349,8 +359,22 @@ def run_path(torch, w, dws, residuals, h0, state, uniform_k, steps, warmup, ev: 
     return out
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, host, seconds):
-    """Time the oracle (as it is) on a bounded sample of the workload."""
+    """Time the oracle (as it is) on a bounded sample of the workload: the whole layer
+    (router, budget, TopK, permutation, experts, combine) and, separately, its routing
+    half (budget, router, TopK, permutation)."""
     import numpy as np
     import oracle
     try:
@@ -358,6 +382,10 @@ def cpu_baseline(w, host, seconds):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = 1
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):  # pragma: no cover
+        affinity = os.cpu_count() or 1
     wg, wu, wd = host["w_gate"], host["w_up"], host["w_down"]
     wof = lambda e: (wg[e], wu[e], wd[e])  # noqa: E731
     n_sample = w.T if w.T <= 4096 else 1024
@@ -380,13 +408,17 @@ def cpu_baseline(w, host, seconds):
         reps += 1
         if c - t_start >= seconds:
             break
-    per_layer = (t_route + t_exp * (w.T / n_sample)) / reps
+    route_s = t_route / reps
+    per_layer = route_s + (t_exp / reps) * (w.T / n_sample)
     sample = (f"{reps} full oracle layer(s) of {w.name}" if toks is None else
-              f"{reps} rep(s): routing on all {w.T} tokens, experts+combine on {n_sample} sampled "
-              f"tokens, scaled to {w.T}")
+              f"{reps} rep(s) of layer 0 of {w.name}: routing on all {w.T} tokens, experts+combine "
+              f"on {n_sample} sampled tokens, scaled to {w.T}")
     return {"value": round(w.T / per_layer, 2), "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle", "sample": sample + f"; {w.n_layers} layer(s) per step counted",
-            "seconds": round(t_route + t_exp, 2)}
+            "seconds": round(t_route + t_exp, 2), "affinity_cores": int(affinity),
+            "blas_threads": int(threads), "cpu_model": _cpu_model(),
+            "layer_ms": round(per_layer * 1e3, 2), "routing_ms": round(route_s * 1e3, 2),
+            "routing_tokens_per_s": round(w.T / route_s, 1)}
 
 
 def trajectory_stats(a, torch):
@@ -438,8 +470,6 @@ def main():
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the pass that evicts the Infinity Cache (a 512 MiB read) before "
                          "each step")
-    ap.add_argument("--packed-weights", action="store_true",
-                    help="pack the expert weights once (reflex_pack_*) and stream the packed layout")
     ap.add_argument("--trajectory", action="store_true",
                     help="run a synthetic multi-forward decoding trajectory (all blocks, from an "
                          "all-masked start) and print its forward and pair statistics instead")
@@ -449,7 +479,7 @@ def main():
                                                       "COPY_WRITE_CSV"),
                     help="store HBM traffic per GEMM launch from rocprofv3 counter CSVs (no GPU)")
     a = ap.parse_args()
-    layout = "packed at load" if a.packed_weights else "row-major"
+    layout = "row-major"
     if a.ingest_pmc:
         from synth import make_workload
         ingest_pmc(a.workload, layout, *a.ingest_pmc,
@@ -487,13 +517,7 @@ def main():
         dv["router_bias"] = None if w.router_bias is None else to_device(w.router_bias)
         if host["shared"] is not None:
             dv["ws_gate"], dv["ws_up"], dv["ws_down"] = (to_device(x) for x in host["shared"])
-        # with --packed-weights the static weights are packed once, as at model load,
-        # and the timed forwards stream the packed copies (row-major ones dropped)
-        ew = ExpertWeights(**dv)
-        if a.packed_weights:
-            ew.pack()
-            ew.w_gate = ew.w_up = ew.w_down = None
-        dws.append(ew)
+        dws.append(ExpertWeights(**dv))
         hosts.append(host if l == 0 else None)
         if l > 0:
             w.release(l)

@@ -237,8 +237,11 @@ int reflex_topk_variable(const float* logits, const int32_t* k, int T, int E, in
                          float* pair_weight, int32_t pair_capacity, void* stream);
 
 /*
- * Group the P expert-token pairs by expert: a stable counting sort of the
- * token-major pair list by expert, so rows are ordered by (expert, token).
+ * Group the selected expert-token pairs by expert.  The pairs are those of
+ * Section 3.2: token i contributes one pair per selected expert, P = sum_i k_i in
+ * all, and each pair is one row of the routed experts' work in Eq. (2).  A stable
+ * counting sort of the token-major pair list by expert orders the rows by
+ * (expert, token), so every expert's rows are contiguous for its GEMM.
  *  pair_offsets [T+1] int32, pair_expert [P] int32   from reflex_topk_variable
  *  pairs        [1]   int32  device P (clamped to pair_capacity)
  *  expert_offsets [E+1] int32  output: rows of expert e are
@@ -270,24 +273,6 @@ int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
                           const uint16_t* w_up, const uint16_t* w_down, int T, int E, int d,
                           int f, int32_t pair_capacity, uint16_t* y_sorted, void* ws,
                           size_t ws_bytes, void* stream);
-
-/*
- * One-time weight pre-packing for the grouped GEMM (done once per model load, like
- * any weight format conversion).  The packed layout stores, for every expert, N
- * tile and 64-wide K step, the weight slice the GEMM stages in LDS as one contiguous
- * 32 KB block, so the GEMM streams its weights sequentially from HBM.  The layout is
- * internal to this library version; only pass buffers written by these functions.
- *  reflex_pack_gate_up: w_gate, w_up [E, f, d] bf16 -> dst of
- *                       reflex_packed_gate_up_size(E, f, d) bytes
- *  reflex_pack_down:    w_down [E, d, f] bf16 -> dst of reflex_packed_down_size(E, d, f)
- * Sizes return 0 for invalid shapes.  Errors: NULL or misaligned pointers, shapes as
- * for reflex_grouped_swiglu.
- */
-size_t reflex_packed_gate_up_size(int E, int f, int d);
-size_t reflex_packed_down_size(int E, int d, int f);
-int reflex_pack_gate_up(const uint16_t* w_gate, const uint16_t* w_up, int E, int f, int d,
-                        uint16_t* dst, void* stream);
-int reflex_pack_down(const uint16_t* w_down, int E, int d, int f, uint16_t* dst, void* stream);
 
 /*
  * Weighted combine (Eq. (2)): out[i] = sum over the pairs j of token i, in rank
@@ -338,10 +323,6 @@ typedef struct {
   const float    *conf_prev1, *conf_prev2;
   const int32_t  *k_in;                      /* [T] or NULL                              */
   const uint16_t *residual_a, *residual_b;   /* [T, d] bf16 added before rounding, or NULL */
-  const uint16_t *w_gate_up_packed;          /* reflex_pack_gate_up output, or NULL; when
-                                                given, w_gate and w_up may be NULL       */
-  const uint16_t *w_down_packed;             /* reflex_pack_down output, or NULL; when
-                                                given, w_down may be NULL                */
   reflex_alloc_params params;
   uint16_t *out;                             /* [T, d] bf16                              */
   int32_t  *k_out;                           /* [T] counts used, or NULL                 */

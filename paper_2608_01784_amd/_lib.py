@@ -30,8 +30,7 @@ class AllocParamsC(ctypes.Structure):
 
 _ARG_PTRS = ["h", "w_gate", "w_up", "w_down", "ws_gate", "ws_up", "ws_down", "w_router",
              "router_bias", "block_idx", "seq_offsets", "active_block", "masked", "hist_len",
-             "conf_prev1", "conf_prev2", "k_in", "residual_a", "residual_b",
-             "w_gate_up_packed", "w_down_packed"]
+             "conf_prev1", "conf_prev2", "k_in", "residual_a", "residual_b"]
 _OUT_PTRS = ["out", "k_out", "pairs_out", "logits_out"]
 
 
@@ -67,10 +66,6 @@ _SIGS = {
     "reflex_grouped_swiglu": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_int32, c_void_p, c_void_p,
                                                                      c_size_t, c_void_p]),
     "reflex_combine": (c_int, [c_void_p] * 5 + [c_int, c_int, c_int32, c_void_p, c_void_p]),
-    "reflex_packed_gate_up_size": (c_size_t, [c_int] * 3),
-    "reflex_packed_down_size": (c_size_t, [c_int] * 3),
-    "reflex_pack_gate_up": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p]),
-    "reflex_pack_down": (c_int, [c_void_p, c_int, c_int, c_int, c_void_p, c_void_p]),
     "reflex_moe_forward": (c_int, [ctypes.POINTER(MoeArgsC), c_void_p, c_size_t, c_void_p]),
     "reflex_moe_forward_timed": (c_int, [ctypes.POINTER(MoeArgsC), c_void_p, c_size_t, c_void_p,
                                          ctypes.POINTER(c_void_p), c_int]),
@@ -247,21 +242,3 @@ def reflex_moe_forward_timed(args: MoeArgsC, ws, events, stream=None):
            "reflex_moe_forward_timed")
 
 
-def reflex_packed_gate_up_size(E, f, d) -> int:
-    return lib().reflex_packed_gate_up_size(E, f, d)
-
-
-def reflex_packed_down_size(E, d, f) -> int:
-    return lib().reflex_packed_down_size(E, d, f)
-
-
-def reflex_pack_gate_up(w_gate, w_up, dst, stream=None):
-    E, f, d = w_gate.shape
-    _check(lib().reflex_pack_gate_up(ptr(w_gate), ptr(w_up), E, f, d, ptr(dst), stream_handle(stream)),
-           "reflex_pack_gate_up")
-
-
-def reflex_pack_down(w_down, dst, stream=None):
-    E, d, f = w_down.shape
-    _check(lib().reflex_pack_down(ptr(w_down), E, d, f, ptr(dst), stream_handle(stream)),
-           "reflex_pack_down")

@@ -7,6 +7,7 @@
 
 #include <initializer_list>
 #include <mutex>
+#include <vector>
 
 #include "common.h"
 
@@ -94,15 +95,99 @@ hipStream_t side_stream() {
   return streams[dev];
 }
 
-// The fork and join events of one forward, created per call (so concurrent callers never
-// share one) and released at scope exit; a destroyed event's pending record and waits
-// still complete.
-struct ForkJoin {
+// Fork and join events of the shared-expert side stream.  Each forward borrows one
+// pair from a per-device pool for the duration of the host call and returns it at
+// exit: a wait enqueued on a stream waits for the event's record as of the wait call,
+// so a later re-record by another forward cannot affect it, and concurrent callers
+// never hold the same pair.  Events are created only when the pool of a device is
+// empty (at most one pair per concurrent caller) and kept for the life of the process.
+struct EventPair {
   hipEvent_t fork = nullptr, join = nullptr;
-  ~ForkJoin() {
-    if (fork) (void)hipEventDestroy(fork);
-    if (join) (void)hipEventDestroy(join);
+};
+
+class EventPool {
+ public:
+  bool take(int dev, EventPair& out) {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      std::vector<EventPair>& v = free_[dev];
+      if (!v.empty()) {
+        out = v.back();
+        v.pop_back();
+        return true;
+      }
+    }
+    EventPair e;
+    if (hipEventCreateWithFlags(&e.fork, hipEventDisableTiming) != hipSuccess) return false;
+    if (hipEventCreateWithFlags(&e.join, hipEventDisableTiming) != hipSuccess) {
+      (void)hipEventDestroy(e.fork);
+      return false;
+    }
+    out = e;
+    return true;
   }
+  void give(int dev, const EventPair& e) {
+    std::lock_guard<std::mutex> g(mu_);
+    free_[dev].push_back(e);
+  }
+
+ private:
+  std::mutex mu_;
+  std::vector<EventPair> free_[64];
+};
+
+EventPool& event_pool() {
+  static EventPool* pool = new EventPool();   // never destroyed: outlives every caller
+  return *pool;
+}
+
+// The shared expert's fork off the caller's stream `s` onto the side stream, as a
+// scope guard.  Once fork() has succeeded, every exit from the forward (success or
+// error) leaves `s` ordered after all work enqueued on the side stream by this call:
+// join() does it on the normal path; on an early error return the destructor records
+// the join and makes `s` wait on it (or, should even that fail, waits on the host for
+// the side stream), so the caller may free or reuse the workspace once `s` is done.
+class SideFork {
+ public:
+  explicit SideFork(hipStream_t s) : s_(s) {}
+  SideFork(const SideFork&) = delete;
+  SideFork& operator=(const SideFork&) = delete;
+
+  // true: `side()` now runs after everything enqueued on `s` so far
+  bool fork() {
+    side_ = side_stream();
+    if (side_ == nullptr || hipGetDevice(&dev_) != hipSuccess || dev_ < 0 || dev_ >= 64) return false;
+    if (!event_pool().take(dev_, ev_)) return false;
+    have_ev_ = true;
+    if (hipEventRecord(ev_.fork, s_) != hipSuccess || hipStreamWaitEvent(side_, ev_.fork, 0) != hipSuccess)
+      return false;     // nothing reached the side stream, or it waits on a recorded fork
+    forked_ = true;
+    return true;
+  }
+  hipStream_t side() const { return side_; }
+  bool forked() const { return forked_; }
+
+  int join() {
+    if (!forked_ || joined_) return REFLEX_OK;
+    joined_ = true;
+    if (hipEventRecord(ev_.join, side_) != hipSuccess || hipStreamWaitEvent(s_, ev_.join, 0) != hipSuccess) {
+      (void)hipStreamSynchronize(side_);
+      return REFLEX_ERR_LAUNCH;
+    }
+    return REFLEX_OK;
+  }
+
+  ~SideFork() {
+    (void)join();
+    if (have_ev_) event_pool().give(dev_, ev_);
+  }
+
+ private:
+  hipStream_t s_;
+  hipStream_t side_ = nullptr;
+  int dev_ = -1;
+  EventPair ev_;
+  bool have_ev_ = false, forked_ = false, joined_ = false;
 };
 
 struct Layout {
@@ -306,29 +391,6 @@ int reflex_grouped_swiglu(const uint16_t* h, const int32_t* sorted_token,
                               pair_capacity, y_sorted, ws, static_cast<hipStream_t>(stream));
 }
 
-size_t reflex_packed_gate_up_size(int E, int f, int d) {
-  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return 0;
-  return packed_gate_up_bytes(E, f, d);
-}
-
-size_t reflex_packed_down_size(int E, int d, int f) {
-  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return 0;
-  return packed_down_bytes(E, d, f);
-}
-
-int reflex_pack_gate_up(const uint16_t* w_gate, const uint16_t* w_up, int E, int f, int d,
-                        uint16_t* dst, void* stream) {
-  RFX_TRY(check_ptrs({w_gate, w_up, dst}, 16));
-  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return REFLEX_ERR_SHAPE;
-  return launch_pack_gate_up(w_gate, w_up, E, f, d, dst, static_cast<hipStream_t>(stream));
-}
-
-int reflex_pack_down(const uint16_t* w_down, int E, int d, int f, uint16_t* dst, void* stream) {
-  RFX_TRY(check_ptrs({w_down, dst}, 16));
-  if (!valid_E(E) || !valid_f(f) || !valid_d(d)) return REFLEX_ERR_SHAPE;
-  return launch_pack_down(w_down, E, d, f, dst, static_cast<hipStream_t>(stream));
-}
-
 int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
                    const int32_t* pair_to_sorted, const float* pair_weight,
                    const uint16_t* shared_y, int T, int d, int32_t pair_capacity, uint16_t* out,
@@ -349,11 +411,7 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || fs < 0 || (fs && !valid_f(fs)))
     return REFLEX_ERR_SHAPE;
   if (a->norm_topk != 0 && a->norm_topk != 1) return REFLEX_ERR_PARAM;
-  RFX_TRY(check_ptrs({a->h, a->w_router, a->out, ws}, 16));
-  if (a->w_gate_up_packed) RFX_TRY(check_ptr(a->w_gate_up_packed, 16));
-  else RFX_TRY(check_ptrs({a->w_gate, a->w_up}, 16));
-  if (a->w_down_packed) RFX_TRY(check_ptr(a->w_down_packed, 16));
-  else RFX_TRY(check_ptr(a->w_down, 16));
+  RFX_TRY(check_ptrs({a->h, a->w_router, a->out, ws, a->w_gate, a->w_up, a->w_down}, 16));
   for (const void* p : {static_cast<const void*>(a->residual_a), static_cast<const void*>(a->residual_b)})
     RFX_TRY(check_opt_ptr(p, 16));
   for (const void* p : {static_cast<const void*>(a->router_bias), static_cast<const void*>(a->k_in),
@@ -410,20 +468,10 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // launches, which leave most CUs idle, and joins the caller's stream before the combine.
   // The stage-timed variant keeps it in line, so that its stage time is its own.
   uint16_t* shared_y_buf = fs ? static_cast<uint16_t*>(at(L.shared_y)) : nullptr;
-  ForkJoin fj;
-  bool shared_forked = false;
-  if (fs && ev == nullptr) {
-    hipStream_t side = side_stream();
-    if (side != nullptr && hipEventCreateWithFlags(&fj.fork, hipEventDisableTiming) == hipSuccess &&
-        hipEventCreateWithFlags(&fj.join, hipEventDisableTiming) == hipSuccess) {
-      if (hipEventRecord(fj.fork, s) != hipSuccess || hipStreamWaitEvent(side, fj.fork, 0) != hipSuccess)
-        return REFLEX_ERR_LAUNCH;
-      RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, shared_y_buf,
-                                  at(L.shared_act), side));
-      if (hipEventRecord(fj.join, side) != hipSuccess) return REFLEX_ERR_LAUNCH;
-      shared_forked = true;
-    }
-  }
+  SideFork side(s);      // declared before any early return below: its exit joins
+  if (fs && ev == nullptr && side.fork())
+    RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, shared_y_buf,
+                                at(L.shared_act), side.side()));
   const int32_t* k = a->k_in;
   // small layers: scores and counts in one launch (independent work side by side)
   const bool front = budget && front_fits(T, d);
@@ -487,14 +535,14 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
     RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
                            sorted_token, pair_to_sorted, at(L.perm), static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(4));
-  RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up,
-                           a->w_gate_up_packed, T, E, d, f, cap, gws, s));
+  RFX_TRY(launch_swiglu_up(a->h, sorted_token, expert_offsets, a->w_gate, a->w_up, T, E, d, f,
+                           cap, gws, s));
   RFX_TRY(mark(5));
-  RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, a->w_down_packed, E, d, f, cap, y, gws, s));
+  RFX_TRY(launch_swiglu_down(expert_offsets, a->w_down, E, d, f, cap, y, gws, s));
   RFX_TRY(mark(6));
   const uint16_t* shared_y = nullptr;
-  if (fs && shared_forked) {
-    if (hipStreamWaitEvent(s, fj.join, 0) != hipSuccess) return REFLEX_ERR_LAUNCH;
+  if (fs && side.forked()) {
+    RFX_TRY(side.join());
     shared_y = shared_y_buf;
   } else if (fs) {
     uint16_t* sy = shared_y_buf;

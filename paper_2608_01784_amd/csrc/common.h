@@ -229,18 +229,11 @@ int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
                          uint16_t* y_sorted, void* ws, hipStream_t s);
 // The same in three steps: per-expert M-tile plan, gate/up GEMM, down GEMM.
 int launch_swiglu_plan(const int32_t* expert_offsets, int E, void* ws, hipStream_t s);
-// w_packed (nullable): weights in the packed layout of launch_pack_*; used instead of
-// the row-major weights when given.
 int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32_t* expert_offsets,
-                     const uint16_t* wg, const uint16_t* wu, const uint16_t* w_packed, int T, int E,
-                     int d, int f, int cap, void* ws, hipStream_t s);
-int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, const uint16_t* w_packed,
-                       int E, int d, int f, int cap, uint16_t* y_sorted, void* ws, hipStream_t s);
-size_t packed_gate_up_bytes(int E, int f, int d);
-size_t packed_down_bytes(int E, int d, int f);
-int launch_pack_gate_up(const uint16_t* wg, const uint16_t* wu, int E, int f, int d, uint16_t* dst,
-                        hipStream_t s);
-int launch_pack_down(const uint16_t* wd, int E, int d, int f, uint16_t* dst, hipStream_t s);
+                     const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
+                     void* ws, hipStream_t s);
+int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
+                       int cap, uint16_t* y_sorted, void* ws, hipStream_t s);
 // One dense expert over rows 0..M-1 of x (the always-on shared expert).
 size_t swiglu_dense_ws_bytes(int M, int f);
 int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* wu,

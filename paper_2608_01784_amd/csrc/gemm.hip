@@ -261,10 +261,8 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ expert_offsets, int E,
     int dense_M, const uint16_t* __restrict__ w0,   // UP: W_gate; DOWN: W_down
     const uint16_t* __restrict__ w1,                // UP: W_up
-    size_t w_expert_stride, int K, int N_out, int x_rows, int out_rows, int packed,
+    size_t w_expert_stride, int K, int N_out, int x_rows, int out_rows,
     uint16_t* __restrict__ out) {
-  // packed != 0: w0 holds the weights as per-(expert, N tile, K step) slices, each the
-  // contiguous 32 KB LDS image of the B operand (see pack_weights_kernel)
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = (N_out + BN - 1) / BN;     // the last N tile may be partial
@@ -330,13 +328,6 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
         }
         a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(GM_A_OPS * wv + j);
       }
-      if (packed) {
-        const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
-#pragma unroll
-        for (int j = 0; j < GM_B_OPS; ++j)
-          b_ptr[j] = w0 + slice0 * GM_B_ELEMS + (GM_B_OPS * wv + j) * 512 + lane * 8;
-        return;
-      }
 #pragma unroll
       for (int j = 0; j < GM_B_OPS; ++j) {
         const int r = lane_row(GM_B_OPS * wv + j);
@@ -364,11 +355,10 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
       int kr = kt + ld_rot;
       kr = kr >= nk ? kr - nk : kr;
       const int k0 = kr * GM_BK;
-      const size_t kb = packed ? static_cast<size_t>(kr) * GM_B_ELEMS : static_cast<size_t>(k0);
 #pragma unroll
       for (int j = 0; j < GM_A_OPS; ++j) lds_dma(a_ptr[j] + k0, As + (GM_A_OPS * wv + j) * 512);
 #pragma unroll
-      for (int j = 0; j < GM_B_OPS; ++j) lds_dma(b_ptr[j] + kb, Bs + (GM_B_OPS * wv + j) * 512);
+      for (int j = 0; j < GM_B_OPS; ++j) lds_dma(b_ptr[j] + k0, Bs + (GM_B_OPS * wv + j) * 512);
     };
     for (int s = 0; s < GM_STAGES - 1 && s < n_steps; ++s) issue(s);
     for (int s = 0; s < n_steps; ++s) {
@@ -503,7 +493,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     const uint16_t* __restrict__ x, const int32_t* __restrict__ gather,
     const int32_t* __restrict__ expert_offsets, int E, const uint16_t* __restrict__ w0,
     const uint16_t* __restrict__ w1, size_t w_expert_stride, int K, int N_out, int x_rows,
-    int out_rows, int packed, uint16_t* __restrict__ out) {
+    int out_rows, uint16_t* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = (N_out + BN - 1) / BN;
@@ -570,27 +560,20 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       }
       a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(TL_A_OPS * wave + j);
     }
-    if (packed) {     // packed slices are the LDS images of 64-wide K steps (TL_BK == GM_BK)
-      const size_t slice0 = (static_cast<size_t>(t.expert) * n_tiles + t.n0 / BN) * nk;
 #pragma unroll
-      for (int j = 0; j < TL_B_OPS; ++j)
-        b_ptr[j] = w0 + slice0 * TL_B_ELEMS + (TL_B_OPS * wave + j) * 512 + lane * 8;
-    } else {
-#pragma unroll
-      for (int j = 0; j < TL_B_OPS; ++j) {
-        const int r = lane_row(TL_B_OPS * wave + j);
-        const uint16_t* wb;
-        int wr;
-        if (UP) {
-          wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
-          wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
-        } else {
-          wb = w0 + t.expert * w_expert_stride;
-          wr = t.n0 + r;
-        }
-        wr = wr < N_out ? wr : N_out - 1;
-        b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(TL_B_OPS * wave + j);
+    for (int j = 0; j < TL_B_OPS; ++j) {
+      const int r = lane_row(TL_B_OPS * wave + j);
+      const uint16_t* wb;
+      int wr;
+      if (UP) {
+        wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
+        wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
+      } else {
+        wb = w0 + t.expert * w_expert_stride;
+        wr = t.n0 + r;
       }
+      wr = wr < N_out ? wr : N_out - 1;
+      b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(TL_B_OPS * wave + j);
     }
   };
   // ---- multiply: B sub-tiles as in the 128-row kernel with two wave columns ----
@@ -609,8 +592,8 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   auto dma_a = [&](int j, uint16_t* As_, int k0_) {
     lds_dma(a_ptr[j] + k0_, As_ + (TL_A_OPS * wave + j) * 512);
   };
-  auto dma_b = [&](int j, uint16_t* Bs_, size_t kb_) {
-    lds_dma(b_ptr[j] + kb_, Bs_ + (TL_B_OPS * wave + j) * 512);
+  auto dma_b = [&](int j, uint16_t* Bs_, int k0_) {
+    lds_dma(b_ptr[j] + k0_, Bs_ + (TL_B_OPS * wave + j) * 512);
   };
   setup_loader(0);
   {
@@ -619,9 +602,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
 #pragma unroll
     for (int j = 0; j < TL_A_OPS; ++j) dma_a(j, A0, kr0 * TL_BK);
 #pragma unroll
-    for (int j = 0; j < TL_B_OPS; ++j)
-      dma_b(j, A0 + TL_A_ELEMS,
-            packed ? static_cast<size_t>(kr0) * TL_B_ELEMS : static_cast<size_t>(kr0) * TL_BK);
+    for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, A0 + TL_A_ELEMS, kr0 * TL_BK);
   }
   int s = 0;
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
@@ -655,12 +636,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       int kr = k_next + ld_rot;     // the slice's place in K for the loading tile's rotation
       kr = kr >= nk ? kr - nk : kr;
       const int k0n = kr * TL_BK;
-      const size_t kbn = packed ? static_cast<size_t>(kr) * TL_B_ELEMS : static_cast<size_t>(k0n);
       if (!active) {
 #pragma unroll
         for (int j = 0; j < TL_A_OPS; ++j) dma_a(j, An, k0n);
 #pragma unroll
-        for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, Bn, kbn);
+        for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, Bn, k0n);
         continue;
       }
       const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
@@ -696,7 +676,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         }
         if (kk == 1) {
 #pragma unroll
-          for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, Bn, kbn);
+          for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, Bn, k0n);
         }
         if (kk < 2) {
           // one copy between every two MFMAs: the copies drain at the rate the
@@ -739,47 +719,6 @@ __global__ __launch_bounds__(256) void tile_plan_kernel(const int32_t* __restric
   }
 }
 
-// Packed weight layout: for expert e, N tile n and K step kt, a contiguous slice of
-// GM_B_ELEMS bf16 that is byte for byte the LDS image the GEMM loader builds for
-// the B operand: 8-row groups q of 1 KB, lane L of a group holding row 8q + L/8,
-// logical chunk (L % 8) ^ (4 (q % 2) + L / 16).  UP interleaves per tile the
-// BROWS/2 gate rows and the matching up rows; rows past N repeat row N-1.  A
-// workgroup then streams whole 32 KB slices in order.
-template <bool UP>
-__global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* __restrict__ w0,
-                                                           const uint16_t* __restrict__ w1,
-                                                           int E, int N, int K,
-                                                           uint16_t* __restrict__ dst) {
-  constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
-  const int n_tiles = (N + BN - 1) / BN, nk = K / GM_BK;
-  const size_t units = static_cast<size_t>(E) * n_tiles * nk * (GM_B_ELEMS / 8);
-  for (size_t u = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; u < units;
-       u += static_cast<size_t>(gridDim.x) * 256) {
-    const int within = static_cast<int>(u % (GM_B_ELEMS / 8));
-    size_t slice = u / (GM_B_ELEMS / 8);
-    const int kt = static_cast<int>(slice % nk);
-    slice /= nk;
-    const int nt = static_cast<int>(slice % n_tiles);
-    const int e = static_cast<int>(slice / n_tiles);
-    const int q = within >> 6, L = within & 63;
-    const int r = q * GM_ROWS_PER_OP + L / GM_CH;
-    const int c = (L % GM_CH) ^ ((r / GM_RG) % GM_CH);
-    const uint16_t* src;
-    int row;
-    if (UP) {
-      src = r < GM_BROWS / 2 ? w0 : w1;
-      row = nt * BN + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
-    } else {
-      src = w0;
-      row = nt * BN + r;
-    }
-    row = row < N ? row : N - 1;
-    const uint4 v = *reinterpret_cast<const uint4*>(
-        src + (static_cast<size_t>(e) * N + row) * K + kt * GM_BK + c * 8);
-    *reinterpret_cast<uint4*>(dst + u * 8) = v;
-  }
-}
-
 // One persistent workgroup per CU (the LDS ring admits one per CU), rounded up to
 // a multiple of the XCD count.
 int persistent_grid() {
@@ -790,8 +729,7 @@ int persistent_grid() {
 template <bool UP>
 int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_off,
                 const int32_t* eo, int E, int dense_M, const uint16_t* w0, const uint16_t* w1,
-                size_t stride, int K, int N, int x_rows, int out_rows, int packed, uint16_t* out,
-                hipStream_t s) {
+                size_t stride, int K, int N, int x_rows, int out_rows, uint16_t* out, hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&swiglu_gemm_kernel<UP>),
@@ -801,22 +739,20 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
     attr_set = true;
   }
   hipLaunchKernelGGL(swiglu_gemm_kernel<UP>, dim3(persistent_grid()), dim3(GM_THREADS), GM_LDS, s,
-                     x, gather, tile_off, eo, E, dense_M, w0, w1, stride, K, N, x_rows, out_rows,
-                     packed, out);
+                     x, gather, tile_off, eo, E, dense_M, w0, w1, stride, K, N, x_rows, out_rows, out);
   return launch_status();
 }
 
 // Tall tiles where an expert would average RFX_TALL_MIN_ROWS rows or more at full
 // pair capacity (the MFMAs, not the weight stream, bound such launches).
-bool use_tall(int cap, int E, bool packed) {
-  return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS &&
-         (!packed || TL_BK == GM_BK);
+bool use_tall(int cap, int E) {
+  return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS;
 }
 
 template <bool UP>
 int launch_gemm_tall(const uint16_t* x, const int32_t* gather, const int32_t* eo, int E,
                      const uint16_t* w0, const uint16_t* w1, size_t stride, int K, int N, int x_rows,
-                     int out_rows, int packed, uint16_t* out, hipStream_t s) {
+                     int out_rows, uint16_t* out, hipStream_t s) {
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&swiglu_gemm_tall_kernel<UP>),
@@ -826,7 +762,7 @@ int launch_gemm_tall(const uint16_t* x, const int32_t* gather, const int32_t* eo
     attr_set = true;
   }
   hipLaunchKernelGGL(swiglu_gemm_tall_kernel<UP>, dim3(persistent_grid()), dim3(TL_THREADS), TL_LDS,
-                     s, x, gather, eo, E, w0, w1, stride, K, N, x_rows, out_rows, packed, out);
+                     s, x, gather, eo, E, w0, w1, stride, K, N, x_rows, out_rows, out);
   return launch_status();
 }
 
@@ -852,51 +788,25 @@ static uint16_t* routed_act(void* ws, int E) {
 }
 
 int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32_t* expert_offsets,
-                     const uint16_t* wg, const uint16_t* wu, const uint16_t* w_packed, int T, int E,
-                     int d, int f, int cap, void* ws, hipStream_t s) {
+                     const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
+                     void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, w_packed != nullptr))
-    return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, w_packed ? w_packed : wg, wu,
-                                  static_cast<size_t>(f) * d, d, f, T, cap, w_packed != nullptr,
-                                  routed_act(ws, E), s);
+  if (use_tall(cap, E))
+    return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, wg, wu,
+                                  static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
-                           w_packed ? w_packed : wg, wu, static_cast<size_t>(f) * d, d, f, T, cap,
-                           w_packed != nullptr, routed_act(ws, E), s);
+                           wg, wu, static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
 }
 
-int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, const uint16_t* w_packed,
-                       int E, int d, int f, int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
+int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
+                       int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, w_packed != nullptr))
-    return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E,
-                                   w_packed ? w_packed : wd, nullptr, static_cast<size_t>(d) * f, f,
-                                   d, cap, cap, w_packed != nullptr, y_sorted, s);
+  if (use_tall(cap, E))
+    return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E, wd, nullptr,
+                                   static_cast<size_t>(d) * f, f, d, cap, cap, y_sorted, s);
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
-                            expert_offsets, E, -1, w_packed ? w_packed : wd, nullptr,
-                            static_cast<size_t>(d) * f, f, d, cap, cap, w_packed != nullptr,
-                            y_sorted, s);
-}
-
-size_t packed_gate_up_bytes(int E, int f, int d) {
-  return static_cast<size_t>(E) * ((f + GM_UP_BN - 1) / GM_UP_BN) * (d / GM_BK) * GM_B_ELEMS *
-         sizeof(uint16_t);
-}
-
-size_t packed_down_bytes(int E, int d, int f) {
-  return static_cast<size_t>(E) * ((d + GM_DOWN_BN - 1) / GM_DOWN_BN) * (f / GM_BK) * GM_B_ELEMS *
-         sizeof(uint16_t);
-}
-
-int launch_pack_gate_up(const uint16_t* wg, const uint16_t* wu, int E, int f, int d, uint16_t* dst,
-                        hipStream_t s) {
-  hipLaunchKernelGGL(pack_weights_kernel<true>, dim3(2048), dim3(256), 0, s, wg, wu, E, f, d, dst);
-  return launch_status();
-}
-
-int launch_pack_down(const uint16_t* wd, int E, int d, int f, uint16_t* dst, hipStream_t s) {
-  hipLaunchKernelGGL(pack_weights_kernel<false>, dim3(2048), dim3(256), 0, s, wd, nullptr, E, d, f,
-                     dst);
-  return launch_status();
+                            expert_offsets, E, -1, wd, nullptr, static_cast<size_t>(d) * f, f, d,
+                            cap, cap, y_sorted, s);
 }
 
 int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
@@ -906,9 +816,9 @@ int launch_swiglu_routed(const uint16_t* h, const int32_t* sorted_token,
   if (cap <= 0) return REFLEX_OK;
   int rc = launch_swiglu_plan(expert_offsets, E, ws, s);
   if (rc == REFLEX_OK)
-    rc = launch_swiglu_up(h, sorted_token, expert_offsets, wg, wu, nullptr, T, E, d, f, cap, ws, s);
+    rc = launch_swiglu_up(h, sorted_token, expert_offsets, wg, wu, T, E, d, f, cap, ws, s);
   if (rc == REFLEX_OK)
-    rc = launch_swiglu_down(expert_offsets, wd, nullptr, E, d, f, cap, y_sorted, ws, s);
+    rc = launch_swiglu_down(expert_offsets, wd, E, d, f, cap, y_sorted, ws, s);
   return rc;
 }
 
@@ -917,9 +827,9 @@ int launch_swiglu_dense(const uint16_t* x, const uint16_t* wg, const uint16_t* w
                         hipStream_t s) {
   if (M <= 0) return REFLEX_OK;
   uint16_t* act = static_cast<uint16_t*>(ws);
-  int rc = launch_gemm<true>(x, nullptr, nullptr, nullptr, 1, M, wg, wu, 0, d, f, M, M, 0, act, s);
+  int rc = launch_gemm<true>(x, nullptr, nullptr, nullptr, 1, M, wg, wu, 0, d, f, M, M, act, s);
   if (rc == REFLEX_OK)
-    rc = launch_gemm<false>(act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, 0, f, d, M, M, 0, y, s);
+    rc = launch_gemm<false>(act, nullptr, nullptr, nullptr, 1, M, wd, nullptr, 0, f, d, M, M, y, s);
   return rc;
 }
 

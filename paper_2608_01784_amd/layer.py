@@ -41,21 +41,6 @@ class ExpertWeights:
     ws_gate: Optional[torch.Tensor] = None
     ws_up: Optional[torch.Tensor] = None
     ws_down: Optional[torch.Tensor] = None
-    w_gate_up_packed: Optional[torch.Tensor] = None
-    w_down_packed: Optional[torch.Tensor] = None
-
-    def pack(self) -> "ExpertWeights":
-        """Write the GEMM's packed weight layout (once per model load) and keep it;
-        forwards then stream the packed copies."""
-        E, f, d = self.w_gate.shape
-        dev = self.w_gate.device
-        gu = torch.empty(_lib.reflex_packed_gate_up_size(E, f, d) // 2, dtype=torch.bfloat16, device=dev)
-        dn = torch.empty(_lib.reflex_packed_down_size(E, d, f) // 2, dtype=torch.bfloat16, device=dev)
-        _lib.reflex_pack_gate_up(self.w_gate, self.w_up, gu)
-        _lib.reflex_pack_down(self.w_down, dn)
-        self.w_gate_up_packed, self.w_down_packed = gu, dn
-        self._f = f
-        return self
 
     @property
     def E(self):
@@ -63,7 +48,7 @@ class ExpertWeights:
 
     @property
     def f(self):
-        return self.w_gate.shape[1] if self.w_gate is not None else self._f
+        return self.w_gate.shape[1]
 
     @property
     def f_shared(self):
@@ -103,7 +88,6 @@ class MoELayer:
         P = _lib.ptr
         a.h, a.w_gate, a.w_up, a.w_down = P(h), P(w.w_gate), P(w.w_up), P(w.w_down)
         a.ws_gate, a.ws_up, a.ws_down = P(w.ws_gate), P(w.ws_up), P(w.ws_down)
-        a.w_gate_up_packed, a.w_down_packed = P(w.w_gate_up_packed), P(w.w_down_packed)
         a.w_router, a.router_bias = P(w.w_router), P(w.router_bias)
         if state is not None:
             a.B = state.active_block.shape[0]

@@ -118,3 +118,19 @@ def test_ingest_pmc_missing_kernel_is_an_error(tmp_path, monkeypatch):
     with pytest.raises(SystemExit):
         bench.ingest_pmc("wl", "row-major", str(fetch), str(fetch), str(cf), str(cw))
     assert not os.path.exists(tmp_path / "traffic.json")
+
+
+def test_stage_roofline_credits_only_algorithmic_bytes():
+    import bench
+    d, f, T, E = 2048, 1024, 8192, 64
+    # MFMA-bound stack layer: FLOPs decide, weights + h once are the algorithmic bytes
+    up = bench.stage_roofline("gemm_up", 0.4, d, f, 42826, 64, T, E)
+    assert up["bound"] == "mfma" and up["algorithmic_flops"] == 4 * d * f * 42826
+    assert up["algorithmic_bytes"] == 64 * 2 * f * d * 2 + T * d * 2
+    assert up["overhead_bytes"] == (42826 - T) * d * 2 + 42826 * f * 2
+    assert abs(up["achieved"] - 4 * d * f * 42826 / 0.4e-3 / 1e12) < 0.01
+    # weight-bound single layer: bytes decide, pipeline traffic is not credited
+    dn = bench.stage_roofline("gemm_down", 0.06, d, f, 5106, 64, 1024, E)
+    assert dn["bound"] == "hbm" and dn["algorithmic_bytes"] == 64 * d * f * 2 + 1024 * d * 2
+    assert dn["overhead_bytes"] == 5106 * f * 2 + (5106 - 1024) * d * 2
+    assert dn["frac"] == round(dn["algorithmic_bytes"] / 0.06e-3 / 1e9 / bench.PEAK_HBM_GBS, 4)

@@ -578,35 +578,6 @@ def test_one_expert_takes_every_token(torch, E):
     layer_tolerance_check(out, ref, "one expert")
 
 
-@pytest.mark.parametrize("case", ["lladamoe_t1024_e64", "llada2mini_t4096_e256", "fuzz_d128_f64",
-                                  "fuzz_d384_f192", "tall_d256_f192"])
-def test_packed_weights_give_bitwise_identical_layer(torch, case):
-    # the packed layout only changes where the GEMM reads each weight slice from;
-    # every product and sum is the same, so the outputs must match bit for bit
-    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
-    if case.startswith("fuzz") or case.startswith("tall"):
-        d, f = (int(x[1:]) for x in case.split("_")[1:])
-        if case.startswith("tall"):     # 4 experts with ~1000 rows each
-            w = make_fuzz_workload(400 + d, T=2000, d=d, E=4, f=f, k_max=2)
-        else:
-            w = make_fuzz_workload(300 + d, T=900, d=d, E=12, f=f, k_max=6)
-        dv = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()),
-              "w_down": to_device(w.w_down()), "w_router": to_device(w.w_router()),
-              "router_bias": None if w.router_bias is None else to_device(w.router_bias)}
-    else:
-        w = workload(case)
-        dv = dict(dev_weights(case))
-    outs = []
-    for packed in (False, True):
-        ew = ExpertWeights(**dv)
-        if packed:
-            ew.pack()
-        lay = MoELayer(w.T, w.d, ew, w.params)
-        outs.append(bf16_bits(lay.forward(to_device(w.h), TokenState(**state_tensors(w)))))
-        torch.cuda.synchronize()
-    assert np.array_equal(outs[0], outs[1])
-
-
 def _fuzz_layer(torch, w, k_in=None):
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
     dw = {"w_gate": to_device(w.w_gate()), "w_up": to_device(w.w_up()), "w_down": to_device(w.w_down()),
