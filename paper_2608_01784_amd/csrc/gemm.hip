@@ -34,6 +34,8 @@
 // runs on XCD b % 8), so one expert's tiles share that XCD's L2.  Within an
 // expert the N tiles of one M tile are adjacent, so the workgroups of an XCD
 // working at the same time share each gathered input slice and each weight slice.
+#include <type_traits>
+
 #include "common.h"
 
 namespace rfx {
@@ -253,6 +255,55 @@ __device__ __forceinline__ void store_wave_tile(const f32x16_t (&acc)[2][NT], co
 static_assert(GM_LDS + 8 * (REFLEX_MAX_EXPERTS + 1) + GM_CW * ST_ELEMS * 2 <= 160 * 1024,
               "128-row ring + staging");
 
+// One 32 x 32 output block of a wave: rows row_base + (0..31), columns col_base +
+// (0..31); UP: SiLU(g) u from the gate and up accumulators.  Same lane layout and LDS
+// staging as store_wave_tile (one store instruction writes 16 rows of 64 bytes).
+template <bool UP>
+__device__ __forceinline__ void store_block(const f32x16_t& g, const f32x16_t& u, int row_base,
+                                            int col_base, int row_end, int N_out,
+                                            uint16_t* __restrict__ out, uint16_t* stage) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(stage));
+  const uint32_t wr = base + ((lane & 31) * ST_LD + 4 * (lane >> 5)) * 2;
+  const uint32_t rd = base + ((lane >> 2) * ST_LD + 8 * (lane & 3)) * 2;
+  u32x2_t v[4];
+#pragma unroll
+  for (int gi = 0; gi < 4; ++gi) {
+    float a4[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if (UP) {
+        const float gg = g[4 * gi + h], uu = u[4 * gi + h];
+        const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
+        a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
+      } else {
+        a4[h] = g[4 * gi + h];
+      }
+    }
+    v[gi] = u32x2_t{pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3])};
+  }
+  u32x4_t r0, r1;
+  asm volatile(
+      "ds_write_b64 %2, %4\n\t"
+      "ds_write_b64 %2, %5 offset:16\n\t"
+      "ds_write_b64 %2, %6 offset:32\n\t"
+      "ds_write_b64 %2, %7 offset:48\n\t"
+      "ds_read_b128 %0, %3\n\t"
+      "ds_read_b128 %1, %3 offset:1280\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r0), "=&v"(r1)
+      : "v"(wr), "v"(rd), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3])
+      : "memory");
+  const int rbase = row_base + (lane >> 2);
+  const int col = col_base + 8 * (lane & 3);
+  if (col < N_out) {
+    if (rbase < row_end) *reinterpret_cast<u32x4_t*>(out + static_cast<size_t>(rbase) * N_out + col) = r0;
+    if (rbase + 16 < row_end)
+      *reinterpret_cast<u32x4_t*>(out + static_cast<size_t>(rbase + 16) * N_out + col) = r1;
+  }
+}
+
+
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
 __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
@@ -451,30 +502,29 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
 // ---- tall tiles: 256 rows x 256 weight rows, 8 waves that all load and multiply ----
 //
 // For experts with many rows the MFMAs, not the weight stream, are the bound.  Two
-// waves share each SIMD, each multiplying a 64 x 128 block (4 x 2 waves over the
-// 256 x 256 tile), so one wave's LDS reads, barrier waits and epilogue overlap the
-// other's MFMAs; every wave issues its share of the next slice's global->LDS copies
-// into the ring slot the previous step has just released, one copy between every two
-// MFMAs of the first two K sub-steps.  Issued all at once after the barrier, the 64
-// copies of a step queue up in the texture path and stall both waves of each SIMD
-// until they drain; spread out, they drain while the other wave keeps the matrix
-// core busy (8 % less time on the 16-layer stack's GEMMs, measured).  The M tile is
-// 256 rows, so per expert the tiles are ceil(n_e / 256), counted in LDS at start.
-#ifndef RFX_TALL_BK
-#define RFX_TALL_BK 64
-#endif
-#ifndef RFX_TALL_STAGES
-#define RFX_TALL_STAGES 2
-#endif
+// waves share each SIMD.  The waves form 2 (pair rows) x 4 (weight rows): wave
+// (wm, wn) multiplies pair rows 128 wm .. 128 wm + 127 (four 32-row blocks) by 64
+// weight rows (UP: the 32 gate rows and the 32 matching up rows of activation columns
+// n0 + 32 wn ..; DOWN: weight rows 64 wn ..).  Waves w and w + 4 share a SIMD, so each
+// SIMD holds one wave of each row half: an expert's last tile, whose rows end early,
+// shortens the MFMA stream of all four SIMDs alike (row blocks past the expert's end
+// are skipped), instead of idling some SIMDs while the others run a full tile.  The K
+// loop is instantiated per count of active row blocks, so the common full tile runs
+// straight-line code with no per-block branches.  Every wave issues its share of the
+// next slice's global->LDS copies into the ring slot the previous step has just
+// released, one copy between every two MFMAs of the first two K sub-steps: issued all
+// at once after the barrier, the 64 copies of a step queue up in the texture path and
+// stall both waves of each SIMD until they drain.  The M tile is 256 rows, so per
+// expert the tiles are ceil(n_e / 256), counted in LDS at start.
 #ifndef RFX_TALL_MIN_ROWS
 #define RFX_TALL_MIN_ROWS 512
 #endif
 constexpr int TL_BM = 2 * kGemmBM;
-constexpr int TL_BK = RFX_TALL_BK;
-constexpr int TL_STAGES = RFX_TALL_STAGES;
+constexpr int TL_BK = 64;
 constexpr int TL_WAVES = 8;
 constexpr int TL_THREADS = 64 * TL_WAVES;
-constexpr int TL_NT = 4;                         // 32-row B sub-tiles per wave
+constexpr int TL_MI = 4;                         // 32-row pair blocks per wave
+constexpr int TL_NJ = 2;                         // 32-row weight blocks per wave
 constexpr int TL_CH = TL_BK / 8;
 constexpr int TL_ROWS_PER_OP = 64 / TL_CH;
 constexpr int TL_RG = 16 / TL_CH;
@@ -483,9 +533,9 @@ constexpr int TL_B_ELEMS = GM_BROWS * TL_BK;
 constexpr int TL_STAGE_ELEMS = TL_A_ELEMS + TL_B_ELEMS;
 constexpr int TL_A_OPS = TL_BM / TL_ROWS_PER_OP / TL_WAVES;   // DMA ops per wave per step
 constexpr int TL_B_OPS = GM_BROWS / TL_ROWS_PER_OP / TL_WAVES;
-constexpr size_t TL_LDS = size_t(TL_STAGES) * TL_STAGE_ELEMS * sizeof(uint16_t);
-static_assert(TL_BK == 32 || TL_BK == 64, "tall BK");
-static_assert(GM_BROWS == 256, "tall tiles: two wave columns of 128 weight rows");
+constexpr size_t TL_LDS = size_t(2) * TL_STAGE_ELEMS * sizeof(uint16_t);   // two-slice ring
+static_assert(GM_BROWS == 256, "tall tiles: four wave columns of 64 weight rows");
+static_assert(TL_A_OPS == 4 && TL_B_OPS == 4, "copy interleave: four of each per wave and step");
 static_assert(TL_LDS + 8192 + TL_WAVES * ST_ELEMS * 2 <= 160 * 1024, "tall LDS ring + staging");
 
 template <bool UP>
@@ -529,7 +579,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   if (l_begin >= l_end) return;
   const int n_my = (l_end - l_begin + per_xcd - 1) / per_xcd;
   const int nk = K / TL_BK;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
 
   // ---- copies: op q of the step fills rows ROWS_PER_OP q ..; lane L writes row
   // r = ROWS_PER_OP q + L / CH at slot L % CH, holding chunk (L % CH) ^ ((r / RG) % CH)
@@ -565,30 +615,22 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       const int r = lane_row(TL_B_OPS * wave + j);
       const uint16_t* wb;
       int wr;
-      if (UP) {
+      if (UP) {     // rows [0, 128): gate rows n0 + r; the rest: up rows n0 + r - 128
         wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
         wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
       } else {
         wb = w0 + t.expert * w_expert_stride;
         wr = t.n0 + r;
       }
-      wr = wr < N_out ? wr : N_out - 1;
+      wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
       b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(TL_B_OPS * wave + j);
     }
   };
-  // ---- multiply: B sub-tiles as in the 128-row kernel with two wave columns ----
-  int b_row[TL_NT];
-#pragma unroll
-  for (int j = 0; j < TL_NT; ++j)
-    b_row[j] = UP ? (j < TL_NT / 2 ? wn * (GM_BROWS / 4) + 32 * j
-                                   : GM_BROWS / 2 + wn * (GM_BROWS / 4) + 32 * (j - TL_NT / 2))
-                  : wn * (GM_BROWS / 2) + 32 * j;
-  const int a_row[2] = {wm * 64, wm * 64 + 32};
+  // ---- multiply: pair blocks 128 wm + 32 i, weight blocks b_row[j]
+  const int b_row[TL_NJ] = {UP ? 32 * wn : 64 * wn, UP ? GM_BROWS / 2 + 32 * wn : 64 * wn + 32};
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
-  f32x16_t acc[2][TL_NT];
+  f32x16_t acc[TL_MI][TL_NJ];
 
-  static_assert(TL_STAGES == 2, "interleaved issue assumes a two-slice ring");
-  // the copies of one slice: A ops, then B ops, into ring slot As_/Bs_ at K slice k0_/kb_
   auto dma_a = [&](int j, uint16_t* As_, int k0_) {
     lds_dma(a_ptr[j] + k0_, As_ + (TL_A_OPS * wave + j) * 512);
   };
@@ -597,31 +639,22 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   };
   setup_loader(0);
   {
-    uint16_t* A0 = smem;
     const int kr0 = ld_rot;
 #pragma unroll
-    for (int j = 0; j < TL_A_OPS; ++j) dma_a(j, A0, kr0 * TL_BK);
+    for (int j = 0; j < TL_A_OPS; ++j) dma_a(j, smem, kr0 * TL_BK);
 #pragma unroll
-    for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, A0 + TL_A_ELEMS, kr0 * TL_BK);
+    for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, smem + TL_A_ELEMS, kr0 * TL_BK);
   }
   int s = 0;
-  for (int tile_i = 0; tile_i < n_my; ++tile_i) {
-    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
-                                          n_tiles, out_rows);
-    const bool active = t.row0 + wm * 64 < t.row_end;     // this wave's rows hold pairs
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < TL_NT; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  // The K loop of one tile with NB active pair blocks (0: this wave only copies).
+  auto k_loop = [&](auto nb_c, int tile_i) {
+    constexpr int NB = decltype(nb_c)::value;
     for (int kt = 0; kt < nk; ++kt, ++s) {
       // the slice after this one: the next K step, the next tile's first, or (after the
       // last step of this workgroup) this step's slice again into the idle ring slot,
       // so the issue below never branches and every source address stays in bounds
-      const bool last_k = kt == nk - 1;
       int k_next = kt + 1;
-      if (last_k) {
+      if (kt == nk - 1) {
         if (tile_i + 1 < n_my) {
           setup_loader(tile_i + 1);
           k_next = 0;
@@ -636,7 +669,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       int kr = k_next + ld_rot;     // the slice's place in K for the loading tile's rotation
       kr = kr >= nk ? kr - nk : kr;
       const int k0n = kr * TL_BK;
-      if (!active) {
+      if (NB == 0) {
 #pragma unroll
         for (int j = 0; j < TL_A_OPS; ++j) dma_a(j, An, k0n);
 #pragma unroll
@@ -645,17 +678,19 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       }
       const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
       const uint16_t* Bs = As + TL_A_ELEMS;
-      bf16x8_t af[2][2], bfr[2][TL_NT];
+      bf16x8_t af[2][TL_MI], bfr[2][TL_NJ];
       auto load = [&](int kk, int buf) {
         const int slot = ((2 * kk + fsel) ^ fx) * 8;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-          af[buf][i] = *reinterpret_cast<const bf16x8_t*>(As + (a_row[i] + frow) * TL_BK + slot);
+        for (int i = 0; i < NB; ++i)
+          af[buf][i] = *reinterpret_cast<const bf16x8_t*>(As + (128 * wm + 32 * i + frow) * TL_BK + slot);
 #pragma unroll
-        for (int j = 0; j < TL_NT; ++j)
+        for (int j = 0; j < TL_NJ; ++j)
           bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * TL_BK + slot);
       };
-      constexpr int kReads = 2 + TL_NT, kMfmas = 2 * TL_NT;
+      // (the instruction scheduler is told the order: reads of kk+1, then MFMAs of kk)
+      constexpr int kReads = NB + TL_NJ, kMfmas = NB * TL_NJ;
+      constexpr int kPer = kMfmas / TL_A_OPS > 0 ? kMfmas / TL_A_OPS : 1;
       load(0, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
 #pragma unroll
@@ -664,10 +699,12 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
           load(kk + 1, (kk + 1) & 1);
           __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
         }
+        // weights as the MFMA's A operand: the accumulator is the transposed tile,
+        // so each lane ends up holding 4 consecutive output columns of one row
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NB; ++i)
 #pragma unroll
-          for (int j = 0; j < TL_NT; ++j)
+          for (int j = 0; j < TL_NJ; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
                                                                 acc[i][j], 0, 0, 0);
         if (kk == 0) {
@@ -679,11 +716,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
           for (int j = 0; j < TL_B_OPS; ++j) dma_b(j, Bn, k0n);
         }
         if (kk < 2) {
-          // one copy between every two MFMAs: the copies drain at the rate the
-          // texture path takes them while the matrix cores keep busy
+          // a copy after every kPer MFMAs: the copies drain at the rate the texture
+          // path takes them while the matrix cores keep busy
 #pragma unroll
-          for (int q = 0; q < kMfmas / 2; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          for (int q = 0; q < TL_A_OPS; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);
             __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
           }
         } else {
@@ -691,9 +728,42 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         }
       }
     }
-    if (active)
-      store_wave_tile<UP, TL_NT>(acc, t, wm * 64, UP ? wn * (GM_BROWS / 4) : wn * (GM_BROWS / 2),
-                                 N_out, out, s_stage[wave]);
+  };
+  for (int tile_i = 0; tile_i < n_my; ++tile_i) {
+    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
+                                          n_tiles, out_rows);
+    // pair blocks of this wave's 128 rows that hold pairs (wave-uniform)
+    int rows = t.row_end - t.row0 - 128 * wm;
+    rows = rows < 0 ? 0 : (rows > 128 ? 128 : rows);
+    const int nb = __builtin_amdgcn_readfirstlane((rows + 31) >> 5);
+#pragma unroll
+    for (int i = 0; i < TL_MI; ++i)
+#pragma unroll
+      for (int j = 0; j < TL_NJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    switch (nb) {
+      case 4: k_loop(std::integral_constant<int, 4>{}, tile_i); break;
+      case 3: k_loop(std::integral_constant<int, 3>{}, tile_i); break;
+      case 2: k_loop(std::integral_constant<int, 2>{}, tile_i); break;
+      case 1: k_loop(std::integral_constant<int, 1>{}, tile_i); break;
+      default: k_loop(std::integral_constant<int, 0>{}, tile_i); break;
+    }
+#pragma unroll
+    for (int i = 0; i < TL_MI; ++i) {
+      if (i < nb) {
+        const int rb = t.row0 + 128 * wm + 32 * i;
+        if (UP) {
+          store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out,
+                            s_stage[wave]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < TL_NJ; ++j)
+            store_block<false>(acc[i][j], acc[i][j], rb, t.n0 + 64 * wn + 32 * j, t.row_end, N_out,
+                               out, s_stage[wave]);
+        }
+      }
+    }
   }
   waitcnt_vm<0>();     // the last (unused) copy lands before the workgroup's LDS is released
 }
