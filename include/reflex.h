@@ -334,6 +334,26 @@ typedef struct {
 int reflex_moe_forward(const reflex_moe_args* args, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * reflex_moe_forward for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the same work
+ * on the same kernels, with the workspace taken from a scratch array the library holds
+ * on each device (REFLEX_NOALLOC_SCRATCH_BYTES, reserved when the library is loaded on
+ * that device and held until the process ends).  The call allocates nothing: no
+ * hipMalloc / hipFree, no stream or event creation (the shared expert runs on `stream`,
+ * not on a side stream).  The caller still passes every input and output in `args`.
+ * Layers whose reflex_workspace_size(T, E, d, f, f_shared, kcap) exceeds
+ * REFLEX_NOALLOC_SCRATCH_BYTES are rejected with REFLEX_ERR_WORKSPACE before anything
+ * is launched (96 MiB holds, e.g., one LLaDA-MoE-shaped layer of T = 1024 tokens,
+ * d 2048, E 64, f 1024, k_max 12).  Every call on a device shares that device's scratch
+ * and leaves its contents behind (nothing in it needs to start zeroed): calls whose
+ * work overlaps on one device (other streams, other threads) race on it and must be
+ * serialised by the caller.
+ * Errors: as reflex_moe_forward; REFLEX_ERR_LAUNCH if the scratch cannot be located.
+ */
+#define REFLEX_NOALLOC_SCRATCH_BYTES (96u << 20)
+int reflex_moe_forward_noalloc(const reflex_moe_args* args, void* stream);
+
+/*
  * reflex_moe_forward with timing marks, for benchmarks: identical work, plus
  * hipEventRecord(stage_events[i], stream) at each stage boundary:
  *   0 start, 1 router done (for layers with T < 4096 on the REFLEX budget path one

@@ -69,6 +69,7 @@ _SIGS = {
     "reflex_moe_forward": (c_int, [ctypes.POINTER(MoeArgsC), c_void_p, c_size_t, c_void_p]),
     "reflex_moe_forward_timed": (c_int, [ctypes.POINTER(MoeArgsC), c_void_p, c_size_t, c_void_p,
                                          ctypes.POINTER(c_void_p), c_int]),
+    "reflex_moe_forward_noalloc": (c_int, [ctypes.POINTER(MoeArgsC), c_void_p]),
 }
 
 N_STAGE_EVENTS = 9
@@ -232,6 +233,14 @@ def reflex_combine(y_sorted, pair_offsets, pair_to_sorted, pair_weight, shared_y
 def reflex_moe_forward(args: MoeArgsC, ws, stream=None):
     _check(lib().reflex_moe_forward(ctypes.byref(args), ptr(ws), ws.numel() * ws.element_size(),
                                     stream_handle(stream)), "reflex_moe_forward")
+
+
+NOALLOC_SCRATCH_BYTES = 96 << 20     # REFLEX_NOALLOC_SCRATCH_BYTES
+
+
+def reflex_moe_forward_noalloc(args: MoeArgsC, stream=None):
+    _check(lib().reflex_moe_forward_noalloc(ctypes.byref(args), stream_handle(stream)),
+           "reflex_moe_forward_noalloc")
 
 
 def reflex_moe_forward_timed(args: MoeArgsC, ws, events, stream=None):

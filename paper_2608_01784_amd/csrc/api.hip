@@ -405,7 +405,7 @@ int reflex_combine(const uint16_t* y_sorted, const int32_t* pair_offsets,
 }
 
 static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream,
-                            void* const* ev) {
+                            void* const* ev, bool may_fork = true) {
   if (a == nullptr || ws == nullptr) return REFLEX_ERR_NULL;
   const int T = a->T, E = a->E, d = a->d, f = a->f, fs = a->f_shared;
   if (!valid_T(T) || !valid_E(E) || !valid_d(d) || !valid_f(f) || fs < 0 || (fs && !valid_f(fs)))
@@ -469,7 +469,7 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // The stage-timed variant keeps it in line, so that its stage time is its own.
   uint16_t* shared_y_buf = fs ? static_cast<uint16_t*>(at(L.shared_y)) : nullptr;
   SideFork side(s);      // declared before any early return below: its exit joins
-  if (fs && ev == nullptr && side.fork())
+  if (fs && ev == nullptr && may_fork && side.fork())
     RFX_TRY(launch_swiglu_dense(a->h, a->ws_gate, a->ws_up, a->ws_down, T, d, fs, shared_y_buf,
                                 at(L.shared_act), side.side()));
   const int32_t* k = a->k_in;
@@ -558,6 +558,36 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
 
 int reflex_moe_forward(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream) {
   return moe_forward_impl(a, ws, ws_bytes, stream, nullptr);
+}
+
+// The device scratch of reflex_moe_forward_noalloc: one copy per device, held from the
+// library's load on that device until the process ends.  In host code `scratch` names
+// a host-side stand-in, not device memory: its device address comes from
+// hipGetSymbolAddress, per device, and only that address is ever passed on.
+static __device__ __align__(256) unsigned char scratch[REFLEX_NOALLOC_SCRATCH_BYTES];
+
+// Device address of `scratch` on the current device, looked up once per device (with
+// that device current) and kept; NULL if the lookup fails.
+static void* noalloc_scratch() {
+  static std::mutex mu;
+  static void* ptrs[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> g(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+    ptrs[dev] = p;
+  }
+  return ptrs[dev];
+}
+
+int reflex_moe_forward_noalloc(const reflex_moe_args* a, void* stream) {
+  if (a == nullptr) return REFLEX_ERR_NULL;
+  void* ws = noalloc_scratch();
+  if (ws == nullptr) return REFLEX_ERR_LAUNCH;
+  // the shared expert stays on `stream`: forking it would create a stream and events
+  return moe_forward_impl(a, ws, REFLEX_NOALLOC_SCRATCH_BYTES, stream, nullptr, false);
 }
 
 int reflex_moe_forward_timed(const reflex_moe_args* a, void* ws, size_t ws_bytes, void* stream,
