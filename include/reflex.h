@@ -126,6 +126,24 @@ size_t      reflex_sizeof_moe_args(void);       /* sizeof(reflex_moe_args)      
  * reflex_permute and reflex_grouped_swiglu with pair_capacity = T * k_max. */
 size_t reflex_workspace_size(int T, int E, int d, int f, int f_shared, int k_max);
 size_t reflex_permute_workspace_size(int pair_capacity, int E);
+
+/*
+ * Where reflex_moe_forward (and _timed, _noalloc) leaves the routing of a forward in its
+ * workspace, for inspection once the stream has completed (tests, debugging): byte
+ * offset of `field` in a workspace sized by reflex_workspace_size with the same
+ * arguments (k_max = the forward's pair-capacity count kcap).  The arrays are those of
+ * reflex_topk_variable (pair_offsets [T+1], pair_expert and pair_weight [T * kcap]) and
+ * reflex_permute (expert_offsets [E+1], sorted_token and pair_to_sorted [T * kcap]),
+ * holding the forward's P selected expert-token pairs (Section 3.2).  The layout is
+ * internal to this library version.  Returns (size_t)-1 for invalid sizes or field.
+ */
+#define REFLEX_WS_PAIR_OFFSETS    0
+#define REFLEX_WS_PAIR_EXPERT     1
+#define REFLEX_WS_PAIR_WEIGHT     2
+#define REFLEX_WS_EXPERT_OFFSETS  3
+#define REFLEX_WS_SORTED_TOKEN    4
+#define REFLEX_WS_PAIR_TO_SORTED  5
+size_t reflex_workspace_offset(int T, int E, int d, int f, int f_shared, int k_max, int field);
 size_t reflex_swiglu_workspace_size(int pair_capacity, int E, int f);
 
 /*

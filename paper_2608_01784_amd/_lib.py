@@ -50,6 +50,7 @@ _SIGS = {
     "reflex_sizeof_moe_args": (c_size_t, []),
     "reflex_workspace_size": (c_size_t, [c_int] * 6),
     "reflex_permute_workspace_size": (c_size_t, [c_int, c_int]),
+    "reflex_workspace_offset": (c_size_t, [c_int] * 7),
     "reflex_swiglu_workspace_size": (c_size_t, [c_int, c_int, c_int]),
     "reflex_router_logits": (c_int, [c_void_p] * 4 + [c_int] * 3 + [c_void_p]),
     "reflex_assign_budget": (c_int, [c_void_p] * 7 + [c_int, c_int, ctypes.POINTER(AllocParamsC)]
@@ -228,6 +229,17 @@ def reflex_combine(y_sorted, pair_offsets, pair_to_sorted, pair_weight, shared_y
     _check(lib().reflex_combine(ptr(y_sorted), ptr(pair_offsets), ptr(pair_to_sorted),
                                 ptr(pair_weight), ptr(shared_y), T, d, cap, ptr(out),
                                 stream_handle(stream)), "reflex_combine")
+
+
+WS_FIELDS = {"pair_offsets": 0, "pair_expert": 1, "pair_weight": 2, "expert_offsets": 3,
+             "sorted_token": 4, "pair_to_sorted": 5}
+
+
+def reflex_workspace_offset(T, E, d, f, f_shared, k_max, field: str) -> int:
+    off = lib().reflex_workspace_offset(T, E, d, f, f_shared, k_max, WS_FIELDS[field])
+    if off == ctypes.c_size_t(-1).value:
+        raise ReflexError(-2, "reflex_workspace_offset")
+    return off
 
 
 def reflex_moe_forward(args: MoeArgsC, ws, stream=None):

@@ -284,6 +284,20 @@ size_t reflex_workspace_size(int T, int E, int d, int f, int f_shared, int k_max
   return make_layout(T, E, d, f, f_shared, k_max, L) ? L.total : 0;
 }
 
+size_t reflex_workspace_offset(int T, int E, int d, int f, int f_shared, int k_max, int field) {
+  Layout L;
+  if (!make_layout(T, E, d, f, f_shared, k_max, L)) return static_cast<size_t>(-1);
+  switch (field) {
+    case REFLEX_WS_PAIR_OFFSETS: return L.pair_offsets;
+    case REFLEX_WS_PAIR_EXPERT: return L.pair_expert;
+    case REFLEX_WS_PAIR_WEIGHT: return L.pair_weight;
+    case REFLEX_WS_EXPERT_OFFSETS: return L.expert_offsets;
+    case REFLEX_WS_SORTED_TOKEN: return L.sorted_token;
+    case REFLEX_WS_PAIR_TO_SORTED: return L.pair_to_sorted;
+    default: return static_cast<size_t>(-1);
+  }
+}
+
 size_t reflex_permute_workspace_size(int pair_capacity, int E) {
   if (pair_capacity < 0 || !valid_E(E)) return 0;
   return permute_ws_bytes(pair_capacity, E);

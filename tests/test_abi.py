@@ -72,6 +72,23 @@ def test_workspace_sizes(L):
     assert L.reflex_permute_workspace_size(-1, E) == 0
 
 
+def test_workspace_offsets_lie_inside_the_workspace(L):
+    T, E, d, f, k = 1000, 64, 2048, 1024, 12
+    ws = L.reflex_workspace_size(T, E, d, f, 0, k)
+    cap = T * k
+    sizes = {0: 4 * (T + 1), 1: 4 * cap, 2: 4 * cap, 3: 4 * (E + 1), 4: 4 * cap, 5: 4 * cap}
+    spans = []
+    for field, n in sizes.items():
+        off = L.reflex_workspace_offset(T, E, d, f, 0, k, field)
+        assert off % 256 == 0 and off + n <= ws, field
+        spans.append((off, off + n))
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))     # no two arrays overlap
+    bad = ctypes.c_size_t(-1).value
+    assert L.reflex_workspace_offset(T, E, d, f, 0, k, 6) == bad
+    assert L.reflex_workspace_offset(T, 300, d, f, 0, k, 0) == bad
+
+
 FAKE = 1 << 20           # 16-byte aligned stand-in address, never dereferenced
 MIS = FAKE + 4           # 4-byte aligned only: invalid for vector-accessed data
 ODD = FAKE + 2           # invalid for any 4-byte element type

@@ -609,6 +609,56 @@ def test_fused_route_sort_limit(torch, T):
     layer_tolerance_check(out, ref, f"route sort limit T={T}")
 
 
+def _fused_routing(torch, lay, w):
+    """The fused forward's own pair list and permutation, read from its workspace."""
+    from paper_2608_01784_amd import _lib as L
+    cap = w.T * lay.kcap
+    args = (w.T, w.E, w.d, w.f, w.f_shared, lay.kcap)
+
+    def arr(field, n, dtype):
+        off = L.reflex_workspace_offset(*args, field)
+        return lay.ws[off:off + 4 * n].cpu().numpy().view(dtype)
+
+    return {"pair_offsets": arr("pair_offsets", w.T + 1, np.int32),
+            "pair_expert": arr("pair_expert", cap, np.int32),
+            "pair_weight": arr("pair_weight", cap, np.float32),
+            "expert_offsets": arr("expert_offsets", w.E + 1, np.int32),
+            "sorted_token": arr("sorted_token", cap, np.int32),
+            "pair_to_sorted": arr("pair_to_sorted", cap, np.int32)}
+
+
+@pytest.mark.parametrize("case", ["tiny_t128_e8", "tiny_roles_t128_e8", "lladamoe_t1024_e64",
+                                  "T4096", "T4112"])
+def test_fused_route_and_permutation_bit_exact(torch, case):
+    # the fused forward's TopK pair list and permutation (sorted inside the route launch
+    # for layers up to 16384 (16-token block, expert) counts: the tiny and LLaDA-MoE
+    # layers and T = 4096 at E = 64; by the permutation launches above it, T = 4112)
+    # against the oracle's TopK and permutation on the forward's own fp32 scores
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    if case.startswith("T"):
+        w = make_fuzz_workload(120, T=int(case[1:]), d=128, E=64, f=64, k_max=12)
+        lay, st = _fuzz_layer(torch, w)
+    else:
+        w = workload(case)
+        lay = MoELayer(w.T, w.d, ExpertWeights(**dev_weights(case)), w.params)
+        st = TokenState(**state_tensors(w))
+    lay.forward(to_device(w.h), st)
+    torch.cuda.synchronize()
+    k = lay.k.cpu().numpy()
+    got = _fused_routing(torch, lay, w)
+    route = oracle.topk_route(lay.logits.cpu().numpy().astype(np.float64), k)
+    P = int(route.offsets[-1])
+    assert int(lay.pairs.item()) == P
+    assert np.array_equal(got["pair_offsets"], route.offsets)
+    assert np.array_equal(got["pair_expert"][:P], route.expert)
+    np.testing.assert_allclose(got["pair_weight"][:P], route.weight, rtol=1e-5, atol=0)
+    ref = oracle.pair_permutation(route.token, route.expert, w.E)
+    assert np.array_equal(got["expert_offsets"], ref.expert_offsets)
+    assert np.array_equal(got["sorted_token"][:P], ref.sorted_token)
+    assert np.array_equal(got["pair_to_sorted"][:P], ref.pair_to_sorted)
+    note(f"{case}: P={P} pairs, TopK and permutation bit-exact")
+
+
 def test_fused_consecutive_calls_and_no_pairs(torch):
     # the route launch's completion counter is re-armed by every forward: three forwards
     # in a row on one workspace, with caller counts that differ (the last one all zero,
