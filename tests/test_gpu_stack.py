@@ -4,8 +4,10 @@ layer by layer with teacher forcing.
 One count vector is computed by the first layer's budget and reused by every layer
 (k shared across the forward's MoE layers, Section 3.3); between layers a fixed
 random residual stands in for attention: h_{l+1} = bf16(h_l + MoE_l(h_l) + rho_l).
-Each checked layer is compared on sampled tokens, given the GPU's own input h_l
-and the GPU's fp32 router scores (selection pinned), so errors do not compound.
+Every layer is compared on sampled tokens, given the GPU's own input h_l and the
+GPU's fp32 router scores (selection pinned), so errors do not compound.  The sample
+takes tokens of every refinement role: masked tokens of the active blocks (the ones
+the reallocation of Eq. (9) moves), prompt tokens and the rest.
 """
 from __future__ import annotations
 
@@ -20,8 +22,7 @@ from synth.device import bf16_bits, state_tensors, to_device
 pytestmark = pytest.mark.gpu
 
 NAME = "lladamoe_stack16_t8192"
-CHECKED = (0, 1, 7, 15)
-N_SAMPLE = 128
+PER_ROLE = 128
 
 
 @pytest.fixture(scope="module")
@@ -29,7 +30,10 @@ def torch():
     return require_gpu()
 
 
-def test_stack16_teacher_forced(torch):
+@pytest.fixture(scope="module")
+def stack_run(torch):
+    """The 16-layer forward once on the GPU; host copies of every layer's input and
+    output (bf16 bits), router scores and the shared counts."""
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
     w = make_workload(NAME)
     L = w.n_layers
@@ -45,7 +49,7 @@ def test_stack16_teacher_forced(torch):
     state = TokenState(**state_tensors(w))
     h = [to_device(w.h)]
     k0 = None
-    saved = {}
+    logits = []
     for l in range(L):
         lay.w = layers[l]
         out = torch.empty_like(h[0])
@@ -54,38 +58,66 @@ def test_stack16_teacher_forced(torch):
         if l == 0:
             k0 = lay.k.clone()
             pairs0 = int(lay.pairs.item())
-        if l in CHECKED:
-            saved[l] = lay.logits.cpu().numpy().astype(np.float64)
+        else:
+            assert int(lay.pairs.item()) == pairs0      # the same counts in every layer
+        logits.append(lay.logits.cpu().numpy().astype(np.float64))
         h.append(out)
     torch.cuda.synchronize()
-    note(f"{NAME}: 16 layers run")
+    hb = [bf16_bits(x) for x in h]
+    del layers, res, h
+    note(f"{NAME}: 16 layers run, P = {pairs0} per layer")
+    # sampled tokens of every role
+    rng = np.random.default_rng(3)
+    act = np.zeros(w.T, bool)
+    for s in range(len(w.seq_offsets) - 1):
+        lo, hi = int(w.seq_offsets[s]), int(w.seq_offsets[s + 1])
+        act[lo:hi] = w.block_idx[lo:hi] == w.active_block[s]
+    groups = [np.nonzero(act & (w.masked == 1))[0], np.nonzero(w.block_idx == 0)[0]]
+    groups.append(np.setdiff1d(np.arange(w.T), np.concatenate(groups)))
+    toks = np.sort(np.concatenate([rng.choice(g, min(PER_ROLE, len(g)), replace=False)
+                                   for g in groups]))
+    return {"w": w, "h": hb, "logits": logits, "k": k0.cpu().numpy(), "pairs": pairs0, "toks": toks}
 
-    k = k0.cpu().numpy()
+
+def test_stack16_shared_counts(stack_run):
+    w = stack_run["w"]
     ref_b = oracle_budget(w)
-    assert np.array_equal(k, ref_b.k)
-    assert pairs0 == ref_b.pairs
-    toks = np.sort(np.random.default_rng(3).choice(w.T, N_SAMPLE, replace=False))
-    for l in CHECKED:
-        h_in = bf16_bits(h[l])
-        got = oracle.bf16_to_f64(bf16_bits(h[l + 1])[toks])
+    assert np.array_equal(stack_run["k"], ref_b.k)
+    assert stack_run["pairs"] == ref_b.pairs
+
+
+@pytest.mark.parametrize("first", [0, 4, 8, 12])
+def test_stack16_teacher_forced(stack_run, first):
+    w, hb, toks, k = stack_run["w"], stack_run["h"], stack_run["toks"], stack_run["k"]
+    for l in range(first, first + 4):
+        h_in = hb[l]
+        got = oracle.bf16_to_f64(hb[l + 1][toks])
         r = oracle.router_scores(h_in[toks], w.w_router(l))
-        assert np.all(np.abs(saved[l][toks] - r).max(axis=1) <= 1e-4 * np.abs(r).max(axis=1))
-        route = oracle.topk_route(saved[l], k, w.norm_topk)
-        moe = oracle.moe_layer(h_in, route, lambda e, l=l: w.expert_weights(l, e), w.E,
-                               tokens=toks)
+        s = stack_run["logits"][l]
+        assert np.all(np.abs(s[toks] - r).max(axis=1) <= 1e-4 * np.abs(r).max(axis=1))
+        route = oracle.topk_route(s, k, w.norm_topk)
+        moe = oracle.moe_layer(h_in, route, lambda e, l=l: w.expert_weights(l, e), w.E, tokens=toks)
         ref = moe + oracle.bf16_to_f64(h_in[toks]) + oracle.bf16_to_f64(w.residual(l)[toks])
-        layer_tolerance_check(got, ref, f"{NAME} layer {l} (teacher forced)")
-    # end-to-end drift is reported, not asserted: the stack compounds 16 roundings
-    h_last = oracle.bf16_to_f64(bf16_bits(h[L])[toks])
-    note(f"{NAME}: |h_16| rms {np.sqrt((h_last ** 2).mean()):.3f}")
+        layer_tolerance_check(got, ref, f"{NAME} layer {l} ({len(toks)} tokens, teacher forced)")
+    if first == 12:
+        # end-to-end drift is reported, not asserted: the stack compounds 16 roundings
+        h_last = oracle.bf16_to_f64(hb[16][toks])
+        note(f"{NAME}: |h_16| rms {np.sqrt((h_last ** 2).mean()):.3f}")
 
 
-def test_per_layer_counts(torch):
+@pytest.mark.parametrize("case", ["fuzz", "lladamoe"])
+def test_per_layer_counts(torch, case):
     # counts given per layer as rows of an [L, T] array (a per-layer allocation,
     # Section 3.3's generalisation); each layer is checked against the oracle with
-    # its own row, teacher forced
+    # its own row, teacher forced: a small fuzzed shape on every token, and three
+    # LLaDA-MoE-shaped layers (T 1024, d 2048, E 64, f 1024) on sampled tokens
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer
-    w = make_fuzz_workload(321, T=700, d=256, E=16, f=128, k_max=6)
+    if case == "fuzz":
+        w = make_fuzz_workload(321, T=700, d=256, E=16, f=128, k_max=6)
+        toks = None
+    else:
+        w = make_workload("lladamoe_t1024_e64")
+        toks = np.sort(np.random.default_rng(4).choice(w.T, 192, replace=False))
     L = 3
     k_rows = np.random.default_rng(9).integers(0, w.params.k_max + 1, (L, w.T)).astype(np.int32)
     k_dev = to_device(k_rows)
@@ -105,10 +137,11 @@ def test_per_layer_counts(torch):
         logits.append(lay.logits.cpu().numpy().astype(np.float64))
         h.append(out)
     torch.cuda.synchronize()
+    rows = slice(None) if toks is None else toks
     for l in range(L):
         h_in = bf16_bits(h[l])
         route = oracle.topk_route(logits[l], k_rows[l])
-        wg, wu, wd = w.w_gate(l), w.w_up(l), w.w_down(l)
-        ref = (oracle.moe_layer(h_in, route, lambda e: (wg[e], wu[e], wd[e]), w.E)
-               + oracle.bf16_to_f64(h_in) + oracle.bf16_to_f64(w.residual(l)))
-        layer_tolerance_check(oracle.bf16_to_f64(bf16_bits(h[l + 1])), ref, f"per-layer counts, layer {l}")
+        ref = (oracle.moe_layer(h_in, route, lambda e, l=l: w.expert_weights(l, e), w.E, tokens=toks)
+               + oracle.bf16_to_f64(h_in[rows]) + oracle.bf16_to_f64(w.residual(l)[rows]))
+        layer_tolerance_check(oracle.bf16_to_f64(bf16_bits(h[l + 1])[rows]), ref,
+                              f"per-layer counts ({case}), layer {l}")
