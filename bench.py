@@ -457,6 +457,60 @@ def trajectory_stats(a, torch):
         "wall_s": round(wall, 3), "pairs_per_forward": stats.pairs}}), flush=True)
 
 
+def dense_reference(a, torch):
+    """The vendor library's dense bf16 GEMM (hipBLASLt through torch.bmm) on batched shapes
+    with the FLOPs of the workload's routed up and down GEMMs: E experts of P/E rows each (P
+    from one variable-K forward), [E, P/E, d] x [E, d, 2f] and [E, P/E, f] x [E, f, d], and
+    one large [P, d] x [d, 2f] product.  A reference point for what a tuned dense GEMM reaches
+    on this chip at these sizes, not a drop-in: no row gather, no SwiGLU, equal rows per
+    expert.  Operands are contiguous (no transposed views)."""
+    from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
+    from synth import make_workload
+    from synth.device import state_tensors, to_device
+    w = make_workload(a.workload, seed=a.seed)
+    E, d, f, T = w.E, w.d, w.f, w.T
+    lay = MoELayer(T, d, ExpertWeights(w_gate=to_device(w.w_gate(0)), w_up=to_device(w.w_up(0)),
+                                       w_down=to_device(w.w_down(0)),
+                                       w_router=to_device(w.w_router(0))), w.params)
+    lay.forward(to_device(w.h), TokenState(**state_tensors(w)))
+    torch.cuda.synchronize()
+    P = int(lay.pairs.item())
+    w.release(0)
+    del lay
+    m = max(1, round(P / E))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(a.seed)
+
+    def rnd(*shape):
+        return (torch.randn(*shape, device="cuda", generator=g) * 0.02).bfloat16()
+
+    def timed(fn, flops, iters=20):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(iters):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / iters
+        tf = flops / (ms * 1e-3) / 1e12
+        return {"ms": round(ms, 5), "tflops": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+
+    out = {"mode": "dense_reference", "workload": w.name, "library": "hipBLASLt (torch.bmm / mm)",
+           "pairs": P, "experts": E, "rows_per_expert": m}
+    xa, wa = rnd(E, m, d), rnd(E, d, 2 * f)
+    out["up_batched"] = timed(lambda: torch.bmm(xa, wa), 2.0 * E * m * d * 2 * f)
+    del xa, wa
+    xb, wb = rnd(E, m, f), rnd(E, f, d)
+    out["down_batched"] = timed(lambda: torch.bmm(xb, wb), 2.0 * E * m * f * d)
+    del xb, wb
+    xc, wc = rnd(P, d), rnd(d, 2 * f)
+    out["up_one_gemm"] = timed(lambda: torch.mm(xc, wc), 2.0 * P * d * 2 * f)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -473,6 +527,9 @@ def main():
     ap.add_argument("--trajectory", action="store_true",
                     help="run a synthetic multi-forward decoding trajectory (all blocks, from an "
                          "all-masked start) and print its forward and pair statistics instead")
+    ap.add_argument("--dense-reference", action="store_true",
+                    help="time the vendor library's dense bf16 GEMM at the workload's routed GEMM "
+                         "sizes (FLOPs) and print that instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only the plain 256 MiB device copy that calibrates the byte counters")
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -504,6 +561,9 @@ def main():
         copy_calibration()
         return
     _lib.lib()
+    if a.dense_reference:
+        dense_reference(a, torch)
+        return
     if a.trajectory:
         trajectory_stats(a, torch)
         return
