@@ -18,9 +18,11 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Work is
  *    enqueued asynchronously; nothing is read back to the host and no call
  *    synchronises.  Calls keep no state between them and may be made from several
- *    threads; the one lasting resource is a second stream per device (non-blocking,
+ *    threads; the lasting resources are a second stream per device (non-blocking,
  *    default priority, created on first use) on which reflex_moe_forward runs the
- *    shared expert beside the routing, ordered against `stream` by events.
+ *    shared expert beside the routing, ordered against `stream` by events from a
+ *    per-device pool (created on first use, reused by later calls), and the device
+ *    scratch of reflex_moe_forward_noalloc.
  *  - Arguments are validated on the host before anything is launched; on error
  *    nothing is launched and a negative status is returned.  No C++ exception
  *    crosses the ABI.
