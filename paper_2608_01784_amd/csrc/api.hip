@@ -219,7 +219,7 @@ bool make_layout(int T, int E, int d, int f, int fs, int kcap, Layout& L) {
   L.sorted_token = take(sizeof(int32_t) * cap);
   L.pair_to_sorted = take(sizeof(int32_t) * cap);
   L.perm = take(permute_ws_bytes(static_cast<int>(cap), E));
-  L.route_hist = take(route_fused_sorts(T, E) ? route_hist_bytes(T, E) : 0);
+  L.route_hist = take(route_fused_sorts(T, E) || route_block_sorts(T, E) ? route_hist_bytes(T, E) : 0);
   L.swiglu = take(swiglu_ws_bytes(static_cast<int>(cap), E, f));
   L.y = take(sizeof(uint16_t) * cap * d);
   L.shared_act = fs ? take(swiglu_dense_ws_bytes(T, fs)) : o;
@@ -475,8 +475,12 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   uint16_t* y = static_cast<uint16_t*>(at(L.y));
   void* gws = at(L.swiglu);
 
-  // the fused route kernel's completion counter, zeroed by the router launch
-  int32_t* done = route_fused_sorts(T, E) ? static_cast<int32_t*>(at(L.done)) : nullptr;
+  // how the pairs get sorted: inside the route launch (its completion counter is zeroed
+  // by the router launch), by the block-sort launches, or by the permutation launches
+  const bool fused_sort = route_fused_sorts(T, E), block_sort = route_block_sorts(T, E);
+  int32_t* done = fused_sort ? static_cast<int32_t*>(at(L.done)) : nullptr;
+  int32_t* route_hist =
+      fused_sort || block_sort ? static_cast<int32_t*>(at(L.route_hist)) : nullptr;
   RFX_TRY(mark(0));
   // The shared expert reads only h: on the side stream it runs beside the routing
   // launches, which leave most CUs idle, and joins the caller's stream before the combine.
@@ -541,11 +545,14 @@ static int moe_forward_impl(const reflex_moe_args* a, void* ws, size_t ws_bytes,
   // plan at the head of gws.
   RFX_TRY(launch_route_fused(scores, n_parts, static_cast<size_t>(T) * E, part_bias, scores_out, k,
                              T, E, kcap, a->norm_topk, pair_offsets, pair_expert,
-                             pair_weight, a->pairs_out, done, static_cast<int32_t*>(at(L.route_hist)),
+                             pair_weight, a->pairs_out, done, route_hist,
                              expert_offsets, sorted_token, pair_to_sorted,
                              static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(3));
-  if (done == nullptr)
+  if (block_sort)
+    RFX_TRY(launch_block_sort(pair_offsets, pair_expert, T, E, cap, route_hist, expert_offsets,
+                              sorted_token, pair_to_sorted, static_cast<int32_t*>(gws), s));
+  else if (!fused_sort)
     RFX_TRY(launch_permute(pair_offsets, pair_expert, pair_offsets + T, T, E, cap, expert_offsets,
                            sorted_token, pair_to_sorted, at(L.perm), static_cast<int32_t*>(gws), s));
   RFX_TRY(mark(4));

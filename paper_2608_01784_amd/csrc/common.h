@@ -199,14 +199,21 @@ int launch_topk(const float* logits, const int32_t* k, int T, int E, int k_max, 
                 const int32_t* pair_offsets, int32_t* pair_expert, float* pair_weight,
                 hipStream_t s);
 
-// Pair offsets + TopK, and the permutation too when route_fused_sorts(T, E) and `done`
-// is a device word the preceding launch set to zero (hist: route_hist_bytes(T, E) of
-// scratch); else done must be NULL and launch_permute follows.  pairs_out nullable.
-// The scores are n_parts partials part_stride floats apart, added in order, plus bias
-// (nullable); n_parts = 1 with bias NULL reads finished scores.  logits_out (nullable)
-// receives the finished scores.
+// Pair offsets + TopK, and the permutation:
+//  - route_fused_sorts(T, E): inside this launch, given hist (route_hist_bytes(T, E) of
+//    scratch) and `done`, a device word the preceding launch set to zero;
+//  - route_block_sorts(T, E): given hist and done NULL, this launch ranks the pairs in
+//    their 16-token blocks (counts expert-major in hist) and launch_block_sort finishes;
+//  - otherwise hist and done NULL, and launch_permute follows.
+// pairs_out nullable.  The scores are n_parts partials part_stride floats apart, added
+// in order, plus bias (nullable); n_parts = 1 with bias NULL reads finished scores.
+// logits_out (nullable) receives the finished scores.
 bool route_fused_sorts(int T, int E);
+bool route_block_sorts(int T, int E);
 size_t route_hist_bytes(int T, int E);
+int launch_block_sort(const int32_t* pair_offsets, const int32_t* pair_expert, int T, int E,
+                      int cap, int32_t* hist, int32_t* expert_offsets, int32_t* sorted_token,
+                      int32_t* pair_to_sorted, int32_t* gemm_tile_off, hipStream_t s);
 int launch_route_fused(const float* logits, int n_parts, size_t part_stride, const float* bias,
                        float* logits_out, const int32_t* k, int T, int E, int k_max,
                        int norm_topk, int32_t* pair_offsets, int32_t* pair_expert,

@@ -620,11 +620,16 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   }
   int my_e = -1;
   if (ki > 0) my_e = topk_select<NX>(row, ki, E, norm_topk, off, pair_expert, pair_weight);
-  if (done == nullptr) return;
+  if (hist == nullptr) return;     // the permutation launches sort the pairs
   if (my_e >= 0) atomicOr(&s_mask[my_e], 1u << wv);
   __syncthreads();
   if (my_e >= 0)       // (token, rank among this workgroup's tokens that chose my_e)
     pair_to_sorted[off + lane] = (i << 5) | __popc(s_mask[my_e] & ((1u << wv) - 1u));
+  if (done == nullptr) {     // the block-sort launches finish: counts expert-major
+    for (int e = tid; e < E; e += RF_WAVES * kWave)
+      hist[static_cast<size_t>(e) * gridDim.x + blockIdx.x] = __popc(s_mask[e]);
+    return;
+  }
   for (int e = tid; e < E; e += RF_WAVES * kWave)
     hist[static_cast<size_t>(blockIdx.x) * E + e] = __popc(s_mask[e]);
   // every wave's stores acknowledged (vmcnt 0, i.e. in this XCD's L2) before the
@@ -738,6 +743,98 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   if (tid == 0) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ------------------------------------------------------------------------------------
+// Block sort (layers above RF_HIST_MAX counts): the route launch has ranked every pair
+// among its 16-token block's pairs of the same expert (pair_to_sorted = token << 5 |
+// rank) and written the blocks' per-expert counts expert-major, cnt[e][b].  Two
+// launches finish the stable (expert, token) order, with no workgroup walking every
+// pair and no cross-workgroup wait:
+//   column scan: workgroup e turns row e of cnt into start rows (the pairs of expert e
+//   in earlier blocks), in place, and writes the expert's total to tot[e];
+//   scatter: every workgroup scans the E totals into expert bases (workgroup 0 also
+//   writes them as expert_offsets, with the GEMM tile plan) and sends each pair of its
+//   block b to base[e] + start[e][b] + rank.
+// ------------------------------------------------------------------------------------
+constexpr int BS_THREADS = 1024;
+constexpr long BS_MAX_COUNTS = 1L << 20;   // (block, expert) counts the block sort takes
+
+__global__ __launch_bounds__(BS_THREADS) void block_colscan_kernel(int32_t* __restrict__ cnt,
+                                                                   int G,
+                                                                   int32_t* __restrict__ tot) {
+  __shared__ int s_wave[BS_THREADS / kWave];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int32_t* row = cnt + static_cast<size_t>(blockIdx.x) * G;
+  int run = 0;     // pairs of this expert in the blocks before the current chunk
+  for (int b0 = 0; b0 < G; b0 += BS_THREADS) {     // uniform across the workgroup
+    const int b = b0 + tid;
+    const int c = b < G ? row[b] : 0;
+    const int incl = wave_inclusive_scan_i32(c, lane);
+    if (lane == 63) s_wave[wv] = incl;
+    __syncthreads();
+    int before = run, chunk = 0;
+#pragma unroll
+    for (int w = 0; w < BS_THREADS / kWave; ++w) {
+      before += w < wv ? s_wave[w] : 0;
+      chunk += s_wave[w];
+    }
+    if (b < G) row[b] = before + incl - c;
+    run += chunk;
+    __syncthreads();     // s_wave is rewritten by the next chunk
+  }
+  if (tid == 0) tot[blockIdx.x] = run;
+}
+
+__global__ __launch_bounds__(256) void block_scatter_kernel(
+    const int32_t* __restrict__ pair_offsets, const int32_t* __restrict__ pair_expert, int T,
+    int cap, int E, int G, const int32_t* __restrict__ start, const int32_t* __restrict__ tot,
+    int32_t* __restrict__ expert_offsets, int32_t* __restrict__ gemm_tile_off,
+    int32_t* __restrict__ sorted_token, int32_t* __restrict__ pair_to_sorted) {
+  __shared__ int s_base[REFLEX_MAX_EXPERTS];
+  __shared__ int s_wave[8];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int t0 = b * RF_WAVES, t1 = min(T, t0 + RF_WAVES);
+  int p0 = pair_offsets[t0], p1 = pair_offsets[t1];
+  // expert bases: exclusive scan of the totals (thread e holds expert e), then this
+  // block's start row added
+  const int n = tid < E ? tot[tid] : 0;
+  const int st = tid < E ? start[static_cast<size_t>(tid) * G + b] : 0;
+  const int incl = wave_inclusive_scan_i32(n, lane);
+  const int tiles = (n + kGemmBM - 1) / kGemmBM;
+  const int tincl = b == 0 ? wave_inclusive_scan_i32(tiles, lane) : 0;
+  if (lane == 63) {
+    s_wave[wv] = incl;
+    s_wave[4 + wv] = tincl;
+  }
+  __syncthreads();
+  if (tid < E) {
+    int eoff = 0, toff = 0;
+    for (int x = 0; x < wv; ++x) {
+      eoff += s_wave[x];
+      toff += s_wave[4 + x];
+    }
+    const int base = eoff + incl - n;
+    s_base[tid] = base + st;
+    if (b == 0) {
+      expert_offsets[tid] = base;
+      if (tid == E - 1) expert_offsets[E] = base + n;
+      gemm_tile_off[tid] = toff + tincl - tiles;
+      if (tid == E - 1) gemm_tile_off[E] = toff + tincl;
+    }
+  }
+  p0 = p0 < 0 ? 0 : (p0 > cap ? cap : p0);
+  p1 = p1 < p0 ? p0 : (p1 > cap ? cap : p1);
+  __syncthreads();
+  for (int p = p0 + tid; p < p1; p += 256) {
+    const int v = pair_to_sorted[p];
+    int e = pair_expert[p];
+    e = e < 0 ? 0 : (e >= E ? E - 1 : e);
+    int pos = s_base[e] + (v & 31);
+    pos = pos < 0 ? 0 : (pos >= cap ? cap - 1 : pos);
+    sorted_token[pos] = v >> 5;
+    pair_to_sorted[p] = pos;
+  }
+}
+
 }  // namespace
 
 int launch_count_rule(const float* logits, int T, int E, int rule, float threshold, int k_min,
@@ -773,8 +870,26 @@ bool route_fused_sorts(int T, int E) {
   return static_cast<long>((T + RF_WAVES - 1) / RF_WAVES) * E <= RF_HIST_MAX;
 }
 
-size_t route_hist_bytes(int T, int E) {
-  return align_up(static_cast<size_t>((T + RF_WAVES - 1) / RF_WAVES) * E * sizeof(int32_t));
+bool route_block_sorts(int T, int E) {
+  const long n = static_cast<long>((T + RF_WAVES - 1) / RF_WAVES) * E;
+  return n > RF_HIST_MAX && n <= BS_MAX_COUNTS;
+}
+
+size_t route_hist_bytes(int T, int E) {     // the counts, and the block sort's E totals
+  return align_up((static_cast<size_t>((T + RF_WAVES - 1) / RF_WAVES) + 1) * E * sizeof(int32_t));
+}
+
+int launch_block_sort(const int32_t* pair_offsets, const int32_t* pair_expert, int T, int E,
+                      int cap, int32_t* hist, int32_t* expert_offsets, int32_t* sorted_token,
+                      int32_t* pair_to_sorted, int32_t* gemm_tile_off, hipStream_t s) {
+  if (T <= 0) return REFLEX_OK;
+  const int G = (T + RF_WAVES - 1) / RF_WAVES;
+  int32_t* tot = hist + static_cast<size_t>(G) * E;
+  hipLaunchKernelGGL(block_colscan_kernel, dim3(E), dim3(BS_THREADS), 0, s, hist, G, tot);
+  hipLaunchKernelGGL(block_scatter_kernel, dim3(G), dim3(256), 0, s, pair_offsets, pair_expert, T,
+                     cap, E, G, hist, tot, expert_offsets, gemm_tile_off, sorted_token,
+                     pair_to_sorted);
+  return launch_status();
 }
 
 int launch_route_fused(const float* logits, int n_parts, size_t part_stride, const float* bias,

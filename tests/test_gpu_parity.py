@@ -597,7 +597,7 @@ def _fuzz_ref(w, logits, k):
 def test_fused_route_sort_limit(torch, T):
     # the fused forward sorts the pairs inside its route launch while (16-token blocks) x
     # experts <= 16384 (T = 4096, E = 64: exactly the limit, 256 workgroups) and with the
-    # permutation launches above it (T = 4112)
+    # block-sort launches above it (T = 4112)
     w = make_fuzz_workload(120, T=T, d=128, E=64, f=64, k_max=12)
     lay, st = _fuzz_layer(torch, w)
     out = oracle.bf16_to_f64(bf16_bits(lay.forward(to_device(w.h), st)))
@@ -628,15 +628,21 @@ def _fused_routing(torch, lay, w):
 
 
 @pytest.mark.parametrize("case", ["tiny_t128_e8", "tiny_roles_t128_e8", "lladamoe_t1024_e64",
-                                  "T4096", "T4112"])
+                                  "T4096", "T4112", "T8192", "T5003E96", "T16384E256",
+                                  "T65536E16"])
 def test_fused_route_and_permutation_bit_exact(torch, case):
-    # the fused forward's TopK pair list and permutation (sorted inside the route launch
-    # for layers up to 16384 (16-token block, expert) counts: the tiny and LLaDA-MoE
-    # layers and T = 4096 at E = 64; by the permutation launches above it, T = 4112)
-    # against the oracle's TopK and permutation on the forward's own fp32 scores
+    # the fused forward's TopK pair list and permutation against the oracle's TopK and
+    # permutation on the forward's own fp32 scores: sorted inside the route launch for
+    # layers up to 16384 (16-token block, expert) counts (the tiny and LLaDA-MoE layers,
+    # T = 4096 at E = 64), by the block-sort launches above (T = 4112, the 16-layer
+    # stack's T = 8192 at E = 64, a ragged T = 5003 at E = 96, the skewed layer's
+    # T = 16384 at E = 256 with up to 16 experts a token, and T = 65536 at E = 16: four
+    # 1024-block chunks per expert column)
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
     if case.startswith("T"):
-        w = make_fuzz_workload(120, T=int(case[1:]), d=128, E=64, f=64, k_max=12)
+        T, _, E = case[1:].partition("E")
+        E = int(E) if E else 64
+        w = make_fuzz_workload(120, T=int(T), d=128, E=E, f=64, k_max=16 if E >= 16 else E)
         lay, st = _fuzz_layer(torch, w)
     else:
         w = workload(case)
@@ -659,11 +665,13 @@ def test_fused_route_and_permutation_bit_exact(torch, case):
     note(f"{case}: P={P} pairs, TopK and permutation bit-exact")
 
 
-def test_fused_consecutive_calls_and_no_pairs(torch):
-    # the route launch's completion counter is re-armed by every forward: three forwards
-    # in a row on one workspace, with caller counts that differ (the last one all zero,
-    # P = 0: an all-zero output), each checked against the oracle
-    w = make_fuzz_workload(121, T=700, d=256, E=16, f=128, k_max=6)
+@pytest.mark.parametrize("T", [700, 4400])
+def test_fused_consecutive_calls_and_no_pairs(torch, T):
+    # the sort's completion counter (the route launch's at T = 700, the block sort's at
+    # T = 4400) is re-armed by every forward: three forwards in a row on one workspace,
+    # with caller counts that differ (the last one all zero, P = 0: an all-zero output),
+    # each checked against the oracle
+    w = make_fuzz_workload(121, T=T, d=256, E=16 if T < 1000 else 64, f=128, k_max=6)
     lay, st = _fuzz_layer(torch, w)
     rng = np.random.default_rng(7)
     for n, k in enumerate([rng.integers(0, 7, w.T), rng.integers(0, 3, w.T), np.zeros(w.T, np.int64)]):
