@@ -570,7 +570,9 @@ __global__ __launch_bounds__(PS_THREADS) void perm_small_kernel(
 constexpr int RF_WAVES = 16;
 constexpr int RF_HIST_MAX = 16384;       // workgroups x experts held in LDS by the last one
 
-template <int NX>
+// SORT: this launch sorts the pairs (its last workgroup, above).  Without it the kernel
+// holds none of that step's LDS tables, so two workgroups fit a CU instead of one.
+template <int NX, bool SORT>
 __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     const float* __restrict__ logits, int n_parts, size_t part_stride,
     const float* __restrict__ bias, float* __restrict__ logits_out,
@@ -625,13 +627,14 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
   __syncthreads();
   if (my_e >= 0)       // (token, rank among this workgroup's tokens that chose my_e)
     pair_to_sorted[off + lane] = (i << 5) | __popc(s_mask[my_e] & ((1u << wv) - 1u));
-  if (done == nullptr) {     // the block-sort launches finish: counts expert-major
+  if (!SORT) {     // the block-sort launches finish: counts expert-major
     for (int e = tid; e < E; e += RF_WAVES * kWave)
       hist[static_cast<size_t>(e) * gridDim.x + blockIdx.x] = __popc(s_mask[e]);
     return;
   }
   for (int e = tid; e < E; e += RF_WAVES * kWave)
     hist[static_cast<size_t>(blockIdx.x) * E + e] = __popc(s_mask[e]);
+  if constexpr (SORT) {
   // every wave's stores acknowledged (vmcnt 0, i.e. in this XCD's L2) before the
   // barrier, so the counter's agent-scope release by thread 0 writes them all back
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -741,6 +744,7 @@ __global__ __launch_bounds__(RF_WAVES * kWave) void route_fused_kernel(
     }
   }
   if (tid == 0) __hip_atomic_store(done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // ------------------------------------------------------------------------------------
@@ -898,11 +902,12 @@ int launch_route_fused(const float* logits, int n_parts, size_t part_stride, con
                        float* pair_weight, int32_t* pairs_out, int32_t* done, int32_t* hist,
                        int32_t* expert_offsets, int32_t* sorted_token, int32_t* pair_to_sorted,
                        int32_t* gemm_tile_off, hipStream_t s) {
-  auto kernel = route_fused_kernel<4>;
+  const bool sort = done != nullptr;
+  auto kernel = sort ? route_fused_kernel<4, true> : route_fused_kernel<4, false>;
   switch (topk_slots(E)) {
-    case 1: kernel = route_fused_kernel<1>; break;
-    case 2: kernel = route_fused_kernel<2>; break;
-    case 3: kernel = route_fused_kernel<3>; break;
+    case 1: kernel = sort ? route_fused_kernel<1, true> : route_fused_kernel<1, false>; break;
+    case 2: kernel = sort ? route_fused_kernel<2, true> : route_fused_kernel<2, false>; break;
+    case 3: kernel = sort ? route_fused_kernel<3, true> : route_fused_kernel<3, false>; break;
     default: break;
   }
   hipLaunchKernelGGL(kernel, dim3((T + RF_WAVES - 1) / RF_WAVES), dim3(RF_WAVES * kWave), 0, s, logits,
