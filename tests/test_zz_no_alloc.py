@@ -91,3 +91,16 @@ def test_noalloc_rejects_layers_beyond_the_scratch(torch):
     with pytest.raises(_lib.ReflexError) as e:
         _lib.reflex_moe_forward_noalloc(args)
     assert e.value.status == -4      # REFLEX_ERR_WORKSPACE, nothing launched
+
+
+def test_noalloc_block_sort_layer(torch):
+    # a layer above the route launch's in-kernel sort (275 blocks of 16 tokens x 64
+    # experts), so the pairs are sorted by the block-sort launches, on the shared scratch;
+    # then the small layer again
+    from synth import make_fuzz_workload
+    w = make_fuzz_workload(140, T=4400, d=256, E=64, f=128, k_max=6)
+    a, b = _both(torch, w, w.T, state_tensors(w), to_device(w.h), weight_tensors(w))
+    _assert_same(a, b, "T=4400 E=64 (block sort)")
+    small = make_workload("tiny_t128_e8")
+    a, b = _both(torch, small, small.T, state_tensors(small), to_device(small.h), weight_tensors(small))
+    _assert_same(a, b, "tiny_t128_e8 after the block-sort layer")
