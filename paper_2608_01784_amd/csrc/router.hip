@@ -117,27 +117,39 @@ __global__ __launch_bounds__(RB_THREADS) void router_big_kernel(const uint16_t* 
     rb_wait<H_OPS + W_OPS, S>(min(S - 2, nk - 1 - kt));   // this wave's copies of slice kt
     __builtin_amdgcn_s_waitcnt(0xc07f);            // lgkmcnt(0)
     asm volatile("s_barrier" ::: "memory");        // slice kt complete; slice kt-1 released
-    if (kt + S - 1 < nk) issue(kt + S - 1);
+    // Every LDS read of slice kt is issued before the copies of the slice S - 1 ahead:
+    // the compiler cannot tell a copy's LDS destination from the slot being read, so a
+    // read placed after a copy would wait for that copy to land (18.8 -> 16.9 us on the
+    // 16-layer stack's router, measured; identical output).
     const uint16_t* H = s_h[kt % S];
     const float* W = s_w[kt % S];
+    const int wr = 16 * wv + frow;                 // this wave's expert row
+    float4 lo4[RB_BK / 32], hi4[RB_BK / 32];
+    bf16x8_t a[RB_BK / 32][TB];
 #pragma unroll
     for (int s32 = 0; s32 < RB_BK / 32; ++s32) {
-      // this wave's expert row 16 wv + frow, K chunk pair (8 s32 + 2g, +1) of 4 fp32 each
-      const int wr = 16 * wv + frow, wc = 8 * s32 + 2 * g;
-      const float4 lo4 = *reinterpret_cast<const float4*>(W + wr * RB_BK + ((wc ^ (wr % 16)) * 4));
-      const float4 hi4 =
-          *reinterpret_cast<const float4*>(W + wr * RB_BK + (((wc + 1) ^ (wr % 16)) * 4));
-      bf16x8_t b0, b1, b2;
-      split3x8(lo4, hi4, b0, b1, b2);
+      // W: K chunk pair (8 s32 + 2g, +1) of 4 fp32 each; h: 16-byte chunk 4 s32 + g
+      const int wc = 8 * s32 + 2 * g;
+      lo4[s32] = *reinterpret_cast<const float4*>(W + wr * RB_BK + ((wc ^ (wr % 16)) * 4));
+      hi4[s32] = *reinterpret_cast<const float4*>(W + wr * RB_BK + (((wc + 1) ^ (wr % 16)) * 4));
 #pragma unroll
       for (int b = 0; b < TB; ++b) {
-        const int hr = 16 * b + frow, hc = 4 * s32 + g;      // 16-byte chunk of the h row
-        const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(H + hr * RB_BK + ((hc ^ ((hr / 2) % 8)) * 8));
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b0, acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b1, acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b2, acc[b], 0, 0, 0);
+        const int hr = 16 * b + frow, hc = 4 * s32 + g;
+        a[s32][b] = *reinterpret_cast<const bf16x8_t*>(H + hr * RB_BK + ((hc ^ ((hr / 2) % 8)) * 8));
       }
+    }
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    // the three split terms in turn over all token blocks: each accumulator still adds
+    // hi, mid, lo of one 32-wide step in that order, TB MFMAs apart instead of one
+#pragma unroll
+    for (int s32 = 0; s32 < RB_BK / 32; ++s32) {
+      bf16x8_t bt[3];
+      split3x8(lo4[s32], hi4[s32], bt[0], bt[1], bt[2]);
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+          acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s32][b], bt[t], acc[b], 0, 0, 0);
     }
   }
   // accumulator: lane l, register r -> token row 4 (l/16) + r, expert column l % 16
