@@ -670,12 +670,8 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
           k_next = kt;
         }
       }
-      // slice s complete and visible; slice s-1 no longer read (a later tile's first
-      // slice was waited for before the previous tile's epilogue)
-      if (kt != 0 || tile_i == 0) {
-        waitcnt_vm<0>();
-        lds_barrier();
-      }
+      waitcnt_vm<0>();
+      lds_barrier();       // slice s complete and visible; slice s-1 no longer read
       uint16_t* An = smem + ((s + 1) & 1) * TL_STAGE_ELEMS;
       uint16_t* Bn = An + TL_A_ELEMS;
       int kr = k_next + ld_rot;     // the slice's place in K for the loading tile's rotation
@@ -760,16 +756,6 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       case 2: k_loop(std::integral_constant<int, 2>{}, tile_i); break;
       case 1: k_loop(std::integral_constant<int, 1>{}, tile_i); break;
       default: k_loop(std::integral_constant<int, 0>{}, tile_i); break;
-    }
-    if (tile_i + 1 < n_my) {
-      // The next tile's first slice, copied during this tile's last step, is waited for
-      // here, before the epilogue.  The vmcnt wait covers a wave's stores as well as its
-      // copies, and every workgroup reaches its epilogue at about the same time, so a
-      // wait after the stores would hold each wave until the chip-wide burst of output
-      // writes drained; placed here, the stores drain during the next slice's MFMAs
-      // (16-layer stack: up + down GEMMs 6 % less time, identical output).
-      waitcnt_vm<0>();
-      lds_barrier();
     }
 #pragma unroll
     for (int i = 0; i < TL_MI; ++i) {
