@@ -6,10 +6,9 @@ namespace rfx {
 namespace {
 
 // ------------------------------------------------------------------------------------
-// TopK: one wave per token.  Lane l holds experts l, l+64, l+128, l+192 as 64-bit
-// keys (order-preserving logit bits << 32 | (0xffff - expert)), so one unsigned
-// max selects the larger logit and, on equal logits, the lower expert index.
-// k_i rounds of wave-wide max pick the experts in rank order.
+// TopK: one wave per token.  Lane l holds experts l, l+64, l+128, l+192 as 32-bit
+// order-preserving keys of their scores; k_i rounds of a wave-wide max pick the
+// experts in rank order.
 // ------------------------------------------------------------------------------------
 constexpr int TK_WAVES = 4;
 
@@ -18,9 +17,9 @@ constexpr int TK_WAVES = 4;
 // slots of 64), topk_select writes the first ki experts in rank order and their
 // weights at pair_expert / pair_weight [o, o + ki) and returns the lane's expert (-1
 // past ki).  Ranking is by score, ties to the lower expert index.  Each round takes the
-// wave maximum of the 32-bit order keys and resolves ties with ballots: the first slot
-// holding the maximum, then its lowest lane, is the lowest expert index.  Consumed
-// experts and lanes past E hold key 0, below every finite score's key.
+// wave maximum of the lanes' largest remaining 32-bit order keys; a ballot names the
+// lane holding it, and equal keys in several lanes go to the lowest expert index.
+// Lanes past E hold key 0, below every finite score's key.
 template <int NX>
 struct TopkRow {
   uint32_t key[NX];
@@ -45,7 +44,7 @@ __device__ __forceinline__ TopkRow<NX> topk_load(const float* __restrict__ row, 
     v[j] = row[e < E ? e : E - 1];
   }
   if (n_parts > 1) {
-    constexpr int PB = 8;     // partials loaded per batch
+    constexpr int PB = 8 / NX > 0 ? 8 / NX : 1;     // partials per batch: 8 loads in flight
     for (int s0 = 1; s0 < n_parts; s0 += PB) {
       float pv[PB][NX];
 #pragma unroll
@@ -83,36 +82,56 @@ __device__ __forceinline__ int topk_select(const TopkRow<NX>& r, int ki, int E, 
                                            int o, int32_t* __restrict__ pair_expert,
                                            float* __restrict__ pair_weight) {
   const int lane = threadIdx.x & 63;
+  // The lane's own keys, sorted once into descending order (equal keys: lower slot,
+  // i.e. lower expert, first), so that a round compares only the lanes' heads: the
+  // wave maximum of the heads is the round's best key, and the lane holding it pops
+  // its head.  A lane's head is its largest remaining key and, among equal ones, its
+  // lowest expert, so the lowest expert among the heads equal to the maximum is the
+  // lowest expert of the whole token with that key.
+  // (the slots of the sorted keys are packed 2 bits each, position x at bits 2x)
   uint32_t key[NX];
+  uint32_t slots = 0;
 #pragma unroll
-  for (int x = 0; x < NX; ++x) key[x] = r.key[x];
-  int my_e = 0;
-  float my_r = 0.0f, rmax = 0.0f;
-  for (int j = 0; j < ki; ++j) {
-    uint32_t best = key[0];
-#pragma unroll
-    for (int x = 1; x < NX; ++x) best = max(best, key[x]);
-    best = wave_max_u32(best);
-    // the winner: the first slot with a lane at the maximum, its lowest such lane
-    int wx = 0;
-    uint64_t wm = __ballot(key[0] == best);
-#pragma unroll
-    for (int x = 1; x < NX; ++x) {
-      const uint64_t m = __ballot(key[x] == best);
-      if (wm == 0) {
-        wm = m;
-        wx = x;
-      }
-    }
-    const int wl = __builtin_ctzll(wm);
-    const int e = wl + kWave * wx;
-    const float v = f32_from_order_key(best);
-#pragma unroll
-    for (int x = 0; x < NX; ++x)        // consume the winner (static indices: registers)
-      key[x] = (lane == wl && x == wx) ? 0u : key[x];
-    if (lane == j) { my_e = e; my_r = v; }
-    if (j == 0) rmax = v;
+  for (int x = 0; x < NX; ++x) {
+    key[x] = r.key[x];
+    slots |= static_cast<uint32_t>(x) << (2 * x);
   }
+#pragma unroll
+  for (int a = 1; a < NX; ++a)          // insertion sort, fully unrolled (registers)
+#pragma unroll
+    for (int b = a; b > 0; --b) {
+      const bool sw = key[b] > key[b - 1];     // strictly greater: ties keep slot order
+      const uint32_t k0 = key[b - 1], k1 = key[b];
+      key[b - 1] = sw ? k1 : k0;
+      key[b] = sw ? k0 : k1;
+      const uint32_t s0 = (slots >> (2 * (b - 1))) & 3u, s1 = (slots >> (2 * b)) & 3u;
+      const uint32_t swapped = (slots & ~(15u << (2 * (b - 1)))) | (s1 << (2 * (b - 1))) | (s0 << (2 * b));
+      slots = sw ? swapped : slots;
+    }
+  int my_e = 0;
+  uint32_t my_key = 0u, top_key = 0u;
+  for (int j = 0; j < ki; ++j) {
+    const uint32_t best = wave_max_u32(key[0]);
+    const uint64_t m = __ballot(key[0] == best);
+    int wl = __builtin_ctzll(m);
+    if (__builtin_popcountll(m) > 1) {
+      // equal heads in several lanes (rare): the lowest expert index among them, as
+      // the wave maximum of the complemented indices
+      const uint32_t c =
+          key[0] == best ? ~static_cast<uint32_t>(lane + kWave * static_cast<int>(slots & 3u)) : 0u;
+      wl = static_cast<int>(~wave_max_u32(c)) & (kWave - 1);
+    }
+    const int e = wl + kWave * static_cast<int>(__builtin_amdgcn_readlane(slots, wl) & 3u);
+    if (lane == wl) {                     // the winner pops its head
+#pragma unroll
+      for (int x = 0; x + 1 < NX; ++x) key[x] = key[x + 1];
+      key[NX - 1] = 0u;
+      slots >>= 2;
+    }
+    if (lane == j) { my_e = e; my_key = best; }
+    if (j == 0) top_key = best;
+  }
+  const float my_r = f32_from_order_key(my_key), rmax = f32_from_order_key(top_key);
   float den;
   if (norm_topk) {
     den = wave_sum_f32(lane < ki ? expf(my_r - rmax) : 0.0f);
@@ -120,7 +139,7 @@ __device__ __forceinline__ int topk_select(const TopkRow<NX>& r, int ki, int E, 
     float part = 0.0f;
 #pragma unroll
     for (int j = 0; j < NX; ++j)
-      if (lane + kWave * j < E) part += expf(r.val[j] - rmax);
+      if (lane + kWave * j < E) part += expf(f32_from_order_key(r.key[j]) - rmax);
     den = wave_sum_f32(part);
   }
   if (lane < ki) {
