@@ -511,6 +511,54 @@ def dense_reference(a, torch):
     print(json.dumps(out), flush=True)
 
 
+def device_figures(torch):
+    """The chip as the runtime reports it, the dense bf16 peak re-derived from that (4096
+    FLOP per clock per CU from the 32x32x16 bf16 MFMA rate of 4 SIMDs), and two measured
+    device-memory rates (plain torch copy and fill of 1 GiB, outside any timed region).
+    The roofline keeps the published peaks; these figures are reported beside them."""
+    p = torch.cuda.get_device_properties(0)
+    cus = int(p.multi_processor_count)
+
+    def attr(code):
+        # hipDeviceGetAttribute of the HIP runtime torch has loaded (ROCm 7 attribute codes:
+        # 5 peak clock kHz, 59 memory bus bits, 60 peak memory clock kHz); 0 if unavailable
+        import ctypes
+        try:
+            hip = ctypes.CDLL("libamdhip64.so")
+            v = ctypes.c_int(0)
+            return v.value if hip.hipDeviceGetAttribute(ctypes.byref(v), code, 0) == 0 else 0
+        except OSError:
+            return 0
+
+    clk_mhz = attr(5) / 1e3
+    out = {"name": p.name, "arch": p.gcnArchName, "cus": cus, "clock_mhz": round(clk_mhz, 1),
+           "l2_bytes": int(p.L2_cache_size), "hbm_bytes": int(p.total_memory),
+           "memory_clock_mhz": round(attr(60) / 1e3, 1), "memory_bus_bits": attr(59),
+           "derived_bf16_tflops": round(4096 * cus * clk_mhz * 1e6 / 1e12, 1)}
+    n = 1 << 29                                      # bf16 elements: 1 GiB
+    x = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    x.fill_(1.0)
+    y = torch.empty_like(x)
+
+    def rate(fn, nbytes, reps=10):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return round(nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+
+    out["measured_copy_gbs"] = rate(lambda: y.copy_(x), 2 * 2 * n)     # 1 GiB read + 1 GiB written
+    out["measured_fill_gbs"] = rate(lambda: y.fill_(0.5), 2 * n)
+    del x, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -601,6 +649,8 @@ def main():
         log("timing fixed-count path (k = K_base)")
         uni = run_path(torch, w, dws, residuals, h0, state, w.params.k_base, a.steps, a.warmup, ev)
     ev.close()
+    log("device figures (runtime properties, 1 GiB copy and fill)")
+    dev = device_figures(torch)
 
     T, d, f, E, L = w.T, w.d, w.f, w.E, w.n_layers
     step_ms = var["wall_ms"]
@@ -632,6 +682,7 @@ def main():
         "step_ms_dist": var["step_dist"],
         "roofline": roof,
         "roofline_all": roof_all,
+        "device": dev,
     }
     if "cold" in var:
         cs = var["cold"]["stage_ms"]
