@@ -629,7 +629,7 @@ def _fused_routing(torch, lay, w):
 
 @pytest.mark.parametrize("case", ["tiny_t128_e8", "tiny_roles_t128_e8", "lladamoe_t1024_e64",
                                   "T4096", "T4112", "T8192", "T5003E96", "T16384E256",
-                                  "T65536E16"])
+                                  "T65536E16", "T4096E256D2048", "T2000E256D2048"])
 def test_fused_route_and_permutation_bit_exact(torch, case):
     # the fused forward's TopK pair list and permutation against the oracle's TopK and
     # permutation on the forward's own fp32 scores: sorted inside the route launch for
@@ -637,12 +637,15 @@ def test_fused_route_and_permutation_bit_exact(torch, case):
     # T = 4096 at E = 64), by the block-sort launches above (T = 4112, the 16-layer
     # stack's T = 8192 at E = 64, a ragged T = 5003 at E = 96, the skewed layer's
     # T = 16384 at E = 256 with up to 16 experts a token, and T = 65536 at E = 16: four
-    # 1024-block chunks per expert column)
+    # 1024-block chunks per expert column).  At d = 2048 the route kernel adds split-K
+    # partial scores as it loads them, here with four slots of experts a lane: the
+    # router's 4 K slices at T = 4096, the front kernel's 8 at T = 2000.
+    import re
     from paper_2608_01784_amd.layer import ExpertWeights, MoELayer, TokenState
     if case.startswith("T"):
-        T, _, E = case[1:].partition("E")
-        E = int(E) if E else 64
-        w = make_fuzz_workload(120, T=int(T), d=128, E=E, f=64, k_max=16 if E >= 16 else E)
+        m = re.fullmatch(r"T(\d+)(?:E(\d+))?(?:D(\d+))?", case)
+        T, E, d = int(m[1]), int(m[2] or 64), int(m[3] or 128)
+        w = make_fuzz_workload(120, T=T, d=d, E=E, f=64, k_max=16 if E >= 16 else E)
         lay, st = _fuzz_layer(torch, w)
     else:
         w = workload(case)
