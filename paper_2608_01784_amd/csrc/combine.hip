@@ -18,17 +18,39 @@ __device__ __forceinline__ void add_bf16x8(float* acc, uint4 v, float w) {
   }
 }
 
-// CB: expert rows in flight per batch.  16 keep a token's rows in one batch on the small
-// layers; from T = 4096 up, 8 (fewer registers, more workgroups resident per CU) are
-// faster (16-layer stack layer: 35.1 against 42.1 us; LLaDA-MoE layer: 7.4 against 7.1).
-template <int CB>
-__global__ __launch_bounds__(256) void combine_kernel(
-    const uint16_t* __restrict__ y, const int32_t* __restrict__ pair_offsets,
+// Expert-output rows are read with the non-temporal hint when what the combine streams
+// (the P expert rows, the token's own rows: residuals and shared expert, and the output)
+// is larger than the 256 MB Infinity Cache: every expert row is read once, and read
+// without the hint the rows evict the lines of the other streams.  Below that size the
+// down GEMM has just written the rows into the cache and the plain loads hit there.
+// Kernel durations traced in one process, identical output: skewed layer (656 MB) 130.3
+// -> 109.3 us; 16-layer stack layer with its two residual streams (276 MB) 51.2 -> 50.1
+// us; with the hint where the streams fit: stack layer without residuals (209 MB) 35.4
+// -> 36.2 us, LLaDA2.0-mini with residuals (152 MB) 28.3 -> 30.3 us.
+constexpr size_t kStreamBytes = size_t(256) << 20;
+
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+
+template <bool STREAM>
+__device__ __forceinline__ uint4 load_row(const uint16_t* p) {
+  if constexpr (STREAM) {
+    const u32x4_nt q = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+    return make_uint4(q.x, q.y, q.z, q.w);
+  } else {
+    return *reinterpret_cast<const uint4*>(p);
+  }
+}
+
+// One token's output row (the body of the kernel below).  CB: expert rows in flight per
+// batch.  16 keep a token's rows in one batch on the small layers; from T = 4096 up, 8
+// (fewer registers, more workgroups resident per CU) are faster (16-layer stack layer:
+// 35.1 against 42.1 us; LLaDA-MoE layer: 7.4 against 7.1).
+template <int CB, bool STREAM>
+__device__ __forceinline__ void combine_token(
+    int i, int p0, int p1, const uint16_t* __restrict__ y,
     const int32_t* __restrict__ pair_to_sorted, const float* __restrict__ pair_weight,
     const uint16_t* __restrict__ shared_y, const uint16_t* __restrict__ res_a,
     const uint16_t* __restrict__ res_b, int d, int cap, uint16_t* __restrict__ out) {
-  const int i = blockIdx.x;
-  int p0 = pair_offsets[i], p1 = pair_offsets[i + 1];
   p0 = p0 < 0 ? 0 : (p0 > cap ? cap : p0);
   p1 = p1 < p0 ? p0 : (p1 > cap ? cap : p1);
   const size_t tok_off = static_cast<size_t>(i) * d;
@@ -55,8 +77,7 @@ __global__ __launch_bounds__(256) void combine_kernel(
       for (int p = p0; p < p1; ++p) {
         int row = pair_to_sorted[p];
         row = row < 0 ? 0 : (row >= cap ? cap - 1 : row);
-        add_bf16x8(acc, *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v),
-                   pair_weight[p]);
+        add_bf16x8(acc, load_row<STREAM>(y + static_cast<size_t>(row) * d + v), pair_weight[p]);
       }
     }
     for (int q = 0; q < (np > kWave ? 0 : np); q += CB) {
@@ -64,7 +85,7 @@ __global__ __launch_bounds__(256) void combine_kernel(
 #pragma unroll
       for (int u = 0; u < CB; ++u) {     // past the count: the last row again, not added
         const int row = __builtin_amdgcn_readlane(prow, min(q + u, np - 1));
-        r[u] = *reinterpret_cast<const uint4*>(y + static_cast<size_t>(row) * d + v);
+        r[u] = load_row<STREAM>(y + static_cast<size_t>(row) * d + v);
       }
 #pragma unroll
       for (int u = 0; u < CB; ++u)
@@ -81,6 +102,29 @@ __global__ __launch_bounds__(256) void combine_kernel(
     o.w = pack_bf16x2(acc[6], acc[7]);
     *reinterpret_cast<uint4*>(out + tok_off + v) = o;
   }
+}
+
+// One workgroup per token (the grid is the T tokens, so pair_offsets[gridDim.x] is the
+// pair count; it is loaded with the token's own offsets, so the choice of load costs no
+// extra round trip).  own: the output row and the token's own input rows.
+template <int CB>
+__global__ __launch_bounds__(256) void combine_kernel(
+    const uint16_t* __restrict__ y, const int32_t* __restrict__ pair_offsets,
+    const int32_t* __restrict__ pair_to_sorted, const float* __restrict__ pair_weight,
+    const uint16_t* __restrict__ shared_y, const uint16_t* __restrict__ res_a,
+    const uint16_t* __restrict__ res_b, int d, int cap, uint16_t* __restrict__ out) {
+  const int i = blockIdx.x;
+  const int p0 = pair_offsets[i], p1 = pair_offsets[i + 1];
+  int P = pair_offsets[gridDim.x];
+  P = P < 0 ? 0 : (P > cap ? cap : P);
+  const size_t own = 1 + (shared_y != nullptr) + (res_a != nullptr) + (res_b != nullptr);
+  const size_t rows = static_cast<size_t>(P) + own * gridDim.x;
+  if (rows * d * sizeof(uint16_t) > kStreamBytes)
+    combine_token<CB, true>(i, p0, p1, y, pair_to_sorted, pair_weight, shared_y, res_a, res_b, d,
+                            cap, out);
+  else
+    combine_token<CB, false>(i, p0, p1, y, pair_to_sorted, pair_weight, shared_y, res_a, res_b, d,
+                             cap, out);
 }
 
 }  // namespace
