@@ -472,7 +472,7 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
           bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * GM_BK + slot);
       };
       // (the instruction scheduler is told the order: reads of kk+1, then MFMAs of kk)
-      constexpr int kReads = 2 + GM_NT, kMfmas = 2 * GM_NT;
+      constexpr int kReads = 2 + GM_NT;
       load(0, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);      // LDS reads
 #pragma unroll
