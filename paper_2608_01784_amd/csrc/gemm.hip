@@ -593,8 +593,14 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   auto lane_row = [&](int q) { return q * TL_ROWS_PER_OP + lane / TL_CH; };
   auto lane_chunk = [&](int q) { return ((lane % TL_CH) ^ ((lane_row(q) / TL_RG) % TL_CH)) * 8; };
   constexpr int CP_OPS = TL_A_OPS;     // copies of each operand per wave and step
-  const uint16_t* a_ptr[CP_OPS];
-  const uint16_t* b_ptr[CP_OPS];
+  // Copy sources as 32-bit element offsets (the host keeps the tall kernel to input
+  // operands of fewer than 2^30 elements): input-row copy j reads x + a_off[j]; the weight
+  // copies of a wave cover 32 consecutive rows of one matrix (gate or up rows in the up
+  // GEMM), so copy j reads b_base + 16 K (j / 2) + b_off[j % 2] (copies j and j + 2 are
+  // 16 rows apart and share the chunk swizzle).
+  uint32_t a_off[CP_OPS];
+  uint32_t b_off[2];
+  const uint16_t* b_base = w0;
   // K rotation: tile (M tile m of its expert, N tile n) walks its K slices starting at
   // slice (2 m + n) mod nk.  The tiles sharing a weight slice (same n) or an input-row
   // slice (same m) then request it one or two steps apart instead of all at once, so
@@ -627,34 +633,45 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         src = gather[src];
         src = src < 0 ? 0 : (src >= x_rows ? x_rows - 1 : src);
       }
-      a_ptr[j] = x + static_cast<size_t>(src) * K + lane_chunk(CP_OPS * wave + j);
+      a_off[j] = static_cast<uint32_t>(src) * static_cast<uint32_t>(K) +
+                 static_cast<uint32_t>(lane_chunk(CP_OPS * wave + j));
     }
+    // the wave's 32 weight rows: tile rows 32 wave .. (UP: 32 (wave % 4) .. of the gate
+    // (waves 0-3) or up (waves 4-7) rows).  N is a multiple of 64 and the rows start at a
+    // multiple of 32, so in a partial last N tile they are all valid or all past N; past
+    // N they are replaced by the last 32 rows (the columns past N are not stored).
+    int wr0 = t.n0 + 32 * (UP ? (wave & 3) : wave);
+    wr0 = wr0 + 32 <= N_out ? wr0 : N_out - 32;
+    const uint16_t* wm_base = (UP && wave >= 4 ? w1 : w0) + t.expert * w_expert_stride;
+    b_base = wm_base + static_cast<size_t>(wr0) * K;
 #pragma unroll
-    for (int j = 0; j < CP_OPS; ++j) {
-      const int r = lane_row(CP_OPS * wave + j);
-      const uint16_t* wb;
-      int wr;
-      if (UP) {     // rows [0, 128): gate rows n0 + r; the rest: up rows n0 + r - 128
-        wb = (r < GM_BROWS / 2 ? w0 : w1) + t.expert * w_expert_stride;
-        wr = t.n0 + (r < GM_BROWS / 2 ? r : r - GM_BROWS / 2);
-      } else {
-        wb = w0 + t.expert * w_expert_stride;
-        wr = t.n0 + r;
-      }
-      wr = wr < N_out ? wr : N_out - 1;     // partial last N tile: columns past N are not stored
-      b_ptr[j] = wb + static_cast<size_t>(wr) * K + lane_chunk(CP_OPS * wave + j);
-    }
+    for (int j = 0; j < 2; ++j)
+      b_off[j] = static_cast<uint32_t>(lane_row(j) * K) +
+                 static_cast<uint32_t>(lane_chunk(CP_OPS * wave + j));
   };
   // ---- multiply: pair blocks 128 wm + 32 i, weight blocks b_row[j]
   const int b_row[TL_NJ] = {UP ? 32 * wn : 64 * wn, UP ? GM_BROWS / 2 + 32 * wn : 64 * wn + 32};
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
   f32x16_t acc[TL_MI][TL_NJ];
 
+  // Input-row copies are buffer loads through a resource of the operand's size.  A copy
+  // that is skipped (wholly past the expert's last row) gets an offset past that size,
+  // which the hardware's range check turns into no memory access, so the step has no
+  // branch: a branch splits the step into several basic blocks, and the instruction order
+  // pinned below then holds only within each (16-layer stack and skewed layer: 2-3 % less
+  // GEMM time than a branch around each copy, identical output; traced in one process).
+  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(x), static_cast<short>(0),
+      static_cast<int>(static_cast<uint32_t>(x_rows) * static_cast<uint32_t>(K) * 2u), 0x00020000);
   auto dma_a = [&](int j, uint16_t* As_, int k0_) {
-    if (j < ld_ops) lds_dma(a_ptr[j] + k0_, As_ + (CP_OPS * wave + j) * 512);
+    const uint32_t voff = j < ld_ops ? (a_off[j] + static_cast<uint32_t>(k0_)) * 2u : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        x_rsrc, (__attribute__((address_space(3))) void*)(As_ + (CP_OPS * wave + j) * 512), 16,
+        voff, 0, 0, kDmaPolicy);
   };
   auto dma_b = [&](int j, uint16_t* Bs_, int k0_) {
-    lds_dma(b_ptr[j] + k0_, Bs_ + (CP_OPS * wave + j) * 512);
+    lds_dma((b_base + k0_ + static_cast<size_t>(16 * (j / 2)) * K) + b_off[j % 2],
+            Bs_ + (CP_OPS * wave + j) * 512);
   };
   setup_loader(0);
   {
@@ -665,10 +682,39 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     for (int j = 0; j < CP_OPS; ++j) dma_b(j, smem + TL_A_ELEMS, kr0 * TL_BK);
   }
   int s = 0;
-  // The K loop of one tile with NB active pair blocks (0: this wave only copies).
+  // The K loop of one tile with NB active pair blocks (0: this wave only copies).  The
+  // MFMAs of each slice's last 16-wide sub-step run after the next step's barrier, from
+  // fragments read before it, so they overlap the LDS reads of the next slice's first
+  // sub-step instead of every SIMD waiting for those reads after each barrier (16-layer
+  // stack and skewed layer: 3-4 % less GEMM time, identical output; traced in one
+  // process).  The fragments stay in the second register buffer across the barrier.
   auto k_loop = [&](auto nb_c, int tile_i) {
     constexpr int NB = decltype(nb_c)::value;
-    for (int kt = 0; kt < nk; ++kt, ++s) {
+    constexpr int kReads = NB + TL_NJ, kMfmas = NB * TL_NJ;
+    constexpr int kPer = kMfmas / CP_OPS > 0 ? kMfmas / CP_OPS : 1;
+    bf16x8_t af[2][TL_MI > 0 ? TL_MI : 1], bfr[2][TL_NJ];
+    // weights as the MFMA's A operand: the accumulator is the transposed tile, so each
+    // lane ends up holding 4 consecutive output columns of one row
+    auto mfmas = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+#pragma unroll
+        for (int j = 0; j < TL_NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[buf][j], af[buf][i], acc[i][j],
+                                                              0, 0, 0);
+    };
+    // a copy after every kPer MFMAs: the copies drain at the rate the texture path takes
+    // them while the matrix cores keep busy
+    auto interleave_copies = [&]() {
+#pragma unroll
+      for (int q = 0; q < CP_OPS; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);
+        __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+      }
+    };
+    // one K step; FIRST: the tile's first, with no deferred MFMAs of a previous slice
+    auto step = [&](auto first_c, int kt) {
+      constexpr bool FIRST = decltype(first_c)::value;
       // the slice after this one: the next K step, the next tile's first, or (after the
       // last step of this workgroup) this step's slice again into the idle ring slot,
       // so the issue below never branches and every source address stays in bounds
@@ -688,65 +734,57 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       int kr = k_next + ld_rot;     // the slice's place in K for the loading tile's rotation
       kr = kr >= nk ? kr - nk : kr;
       const int k0n = kr * TL_BK;
-      if (NB == 0) {
+      if constexpr (NB == 0) {
 #pragma unroll
         for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
 #pragma unroll
         for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
-        continue;
-      }
-      const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
-      const uint16_t* Bs = As + TL_A_ELEMS;
-      bf16x8_t af[2][TL_MI], bfr[2][TL_NJ];
-      auto load = [&](int kk, int buf) {
-        const int slot = ((2 * kk + fsel) ^ fx) * 8;
+      } else {
+        const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
+        const uint16_t* Bs = As + TL_A_ELEMS;
+        auto load = [&](int kk, int buf) {
+          const int slot = ((2 * kk + fsel) ^ fx) * 8;
 #pragma unroll
-        for (int i = 0; i < NB; ++i)
-          af[buf][i] = *reinterpret_cast<const bf16x8_t*>(As + (128 * wm + 32 * i + frow) * TL_BK + slot);
-#pragma unroll
-        for (int j = 0; j < TL_NJ; ++j)
-          bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * TL_BK + slot);
-      };
-      // (the instruction scheduler is told the order: reads of kk+1, then MFMAs of kk)
-      constexpr int kReads = NB + TL_NJ, kMfmas = NB * TL_NJ;
-      constexpr int kPer = kMfmas / CP_OPS > 0 ? kMfmas / CP_OPS : 1;
-      load(0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
-#pragma unroll
-      for (int kk = 0; kk < TL_BK / 16; ++kk) {
-        if (kk + 1 < TL_BK / 16) {
-          load(kk + 1, (kk + 1) & 1);
-          __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
-        }
-        // weights as the MFMA's A operand: the accumulator is the transposed tile,
-        // so each lane ends up holding 4 consecutive output columns of one row
-#pragma unroll
-        for (int i = 0; i < NB; ++i)
+          for (int i = 0; i < NB; ++i)
+            af[buf][i] =
+                *reinterpret_cast<const bf16x8_t*>(As + (128 * wm + 32 * i + frow) * TL_BK + slot);
 #pragma unroll
           for (int j = 0; j < TL_NJ; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[kk & 1][j], af[kk & 1][i],
-                                                                acc[i][j], 0, 0, 0);
-        if (kk == 0) {
+            bfr[buf][j] = *reinterpret_cast<const bf16x8_t*>(Bs + (b_row[j] + frow) * TL_BK + slot);
+        };
+        // (the instruction scheduler is told the order: reads of kk+1, then MFMAs of kk)
+        load(0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+        if constexpr (!FIRST) {
+          mfmas(1);     // the previous slice's last sub-step
 #pragma unroll
           for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
+          interleave_copies();
         }
-        if (kk == 1) {
 #pragma unroll
-          for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
-        }
-        if (kk < 2) {
-          // a copy after every kPer MFMAs: the copies drain at the rate the texture
-          // path takes them while the matrix cores keep busy
+        for (int kk = 0; kk < TL_BK / 16 - 1; ++kk) {
+          load(kk + 1, (kk + 1) & 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+          mfmas(kk & 1);
+          if (FIRST ? kk == 0 : false) {
 #pragma unroll
-          for (int q = 0; q < CP_OPS; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);
-            __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+            for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
           }
-        } else {
-          __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);
+          if (FIRST ? kk == 1 : kk == 0) {
+#pragma unroll
+            for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
+          }
+          if (FIRST ? kk < 2 : kk < 1)
+            interleave_copies();
+          else
+            __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);
         }
       }
-    }
+    };
+    step(std::true_type{}, 0);
+    ++s;
+    for (int kt = 1; kt < nk; ++kt, ++s) step(std::false_type{}, kt);
+    if constexpr (NB > 0) mfmas(1);     // the last slice's last sub-step
   };
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
     const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
@@ -834,8 +872,11 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
 
 // Tall tiles where an expert would average RFX_TALL_MIN_ROWS rows or more at full
 // pair capacity (the MFMAs, not the weight stream, bound such launches).
-bool use_tall(int cap, int E) {
-  return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS;
+// The tall kernel reads its input rows through a buffer resource with 32-bit byte
+// offsets, so its input operand must hold fewer than 2^30 elements.
+bool use_tall(int cap, int E, int x_rows, int K) {
+  return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS &&
+         static_cast<size_t>(x_rows) * static_cast<size_t>(K) < (size_t(1) << 30);
 }
 
 template <bool UP>
@@ -880,7 +921,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
                      const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
                      void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E))
+  if (use_tall(cap, E, T, d))
     return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, wg, wu,
                                   static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
@@ -890,7 +931,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
 int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
                        int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E))
+  if (use_tall(cap, E, cap, f))
     return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E, wd, nullptr,
                                    static_cast<size_t>(d) * f, f, d, cap, cap, y_sorted, s);
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
