@@ -596,11 +596,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   // Copy sources as 32-bit element offsets (the host keeps the tall kernel to input
   // operands of fewer than 2^30 elements): input-row copy j reads x + a_off[j]; the weight
   // copies of a wave cover 32 consecutive rows of one matrix (gate or up rows in the up
-  // GEMM), so copy j reads b_base + 16 K (j / 2) + b_off[j % 2] (copies j and j + 2 are
-  // 16 rows apart and share the chunk swizzle).
+  // GEMM), so copy j reads the wave's rows at 16 K (j / 2) + b_off[j % 2] (copies j and
+  // j + 2 are 16 rows apart and share the chunk swizzle).
   uint32_t a_off[CP_OPS];
   uint32_t b_off[2];
-  const uint16_t* b_base = w0;
+  __amdgpu_buffer_rsrc_t b_rsrc;     // the wave's 32 weight rows of the loading tile
   // K rotation: tile (M tile m of its expert, N tile n) walks its K slices starting at
   // slice (2 m + n) mod nk.  The tiles sharing a weight slice (same n) or an input-row
   // slice (same m) then request it one or two steps apart instead of all at once, so
@@ -643,7 +643,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     int wr0 = t.n0 + 32 * (UP ? (wave & 3) : wave);
     wr0 = wr0 + 32 <= N_out ? wr0 : N_out - 32;
     const uint16_t* wm_base = (UP && wave >= 4 ? w1 : w0) + t.expert * w_expert_stride;
-    b_base = wm_base + static_cast<size_t>(wr0) * K;
+    const uint64_t b_addr = reinterpret_cast<uint64_t>(wm_base + static_cast<size_t>(wr0) * K);
+    const uint64_t b_lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_addr)));
+    const uint64_t b_hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_addr >> 32)));
+    b_rsrc = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(b_lo | (b_hi << 32)),
+                                               static_cast<short>(0), 64 * K, 0x00020000);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       b_off[j] = static_cast<uint32_t>(lane_row(j) * K) +
@@ -654,12 +658,16 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
   f32x16_t acc[TL_MI][TL_NJ];
 
-  // Input-row copies are buffer loads through a resource of the operand's size.  A copy
-  // that is skipped (wholly past the expert's last row) gets an offset past that size,
-  // which the hardware's range check turns into no memory access, so the step has no
-  // branch: a branch splits the step into several basic blocks, and the instruction order
-  // pinned below then holds only within each (16-layer stack and skewed layer: 2-3 % less
-  // GEMM time than a branch around each copy, identical output; traced in one process).
+  // The copies are buffer loads into LDS.  Input rows go through a resource of the
+  // operand's size, and a copy that is skipped (wholly past the expert's last row) gets
+  // an offset past that size, which the hardware's range check turns into no memory
+  // access, so the step has no branch: a branch splits the step into several basic
+  // blocks, and the instruction order pinned below then holds only within each (16-layer
+  // stack and skewed layer: 2-3 % less GEMM time than a branch around each copy,
+  // identical output; traced in one process).  Weight rows go through a resource of the
+  // wave's 32 rows of the tile: with global_load_lds copies the compiler made each
+  // sub-step's MFMAs wait for all of the step's LDS reads, not only their own (2-3 %
+  // less GEMM time with the buffer form).
   const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(x), static_cast<short>(0),
       static_cast<int>(static_cast<uint32_t>(x_rows) * static_cast<uint32_t>(K) * 2u), 0x00020000);
@@ -670,8 +678,10 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         voff, 0, 0, kDmaPolicy);
   };
   auto dma_b = [&](int j, uint16_t* Bs_, int k0_) {
-    lds_dma((b_base + k0_ + static_cast<size_t>(16 * (j / 2)) * K) + b_off[j % 2],
-            Bs_ + (CP_OPS * wave + j) * 512);
+    const uint32_t voff = (b_off[j % 2] + static_cast<uint32_t>(k0_ + 16 * (j / 2) * K)) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        b_rsrc, (__attribute__((address_space(3))) void*)(Bs_ + (CP_OPS * wave + j) * 512), 16,
+        voff, 0, 0, kDmaPolicy);
   };
   setup_loader(0);
   {
