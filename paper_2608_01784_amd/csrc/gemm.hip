@@ -311,6 +311,45 @@ __device__ __forceinline__ void store_block(const f32x16_t& g, const f32x16_t& u
 }
 
 
+// The staging half of store_block for the 256-row kernel: one 32 x 32 block (UP: SiLU(g)
+// u) through the wave's staging buffer into r, rows l/4 and 16 + l/4, columns 8 (l%4)
+// ..+7 of the block, for stores issued later.
+template <bool UP>
+__device__ __forceinline__ void stage_block(const f32x16_t& g, const f32x16_t& u, uint16_t* stage,
+                                            u32x4_t (&r)[2]) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(stage));
+  const uint32_t wr = base + ((lane & 31) * ST_LD + 4 * (lane >> 5)) * 2;
+  const uint32_t rd = base + ((lane >> 2) * ST_LD + 8 * (lane & 3)) * 2;
+  u32x2_t v[4];
+#pragma unroll
+  for (int gi = 0; gi < 4; ++gi) {
+    float a4[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if (UP) {
+        const float gg = g[4 * gi + h], uu = u[4 * gi + h];
+        const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
+        a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
+      } else {
+        a4[h] = g[4 * gi + h];
+      }
+    }
+    v[gi] = u32x2_t{pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3])};
+  }
+  asm volatile(
+      "ds_write_b64 %2, %4\n\t"
+      "ds_write_b64 %2, %5 offset:16\n\t"
+      "ds_write_b64 %2, %6 offset:32\n\t"
+      "ds_write_b64 %2, %7 offset:48\n\t"
+      "ds_read_b128 %0, %3\n\t"
+      "ds_read_b128 %1, %3 offset:1280\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1])
+      : "v"(wr), "v"(rd), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3])
+      : "memory");
+}
+
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
 __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
@@ -657,6 +696,30 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   const int b_row[TL_NJ] = {UP ? 32 * wn : 64 * wn, UP ? GM_BROWS / 2 + 32 * wn : 64 * wn + 32};
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
   f32x16_t acc[TL_MI][TL_NJ];
+  // UP: half of each wave's output (row blocks 2 and 3 of its 4), staged in row layout at
+  // the tile's end, is stored during the next tile's first K step, between its MFMAs,
+  // instead of in the burst in which all workgroups store at once and no MFMAs run
+  // (16-layer stack and skewed layer: 1.0-1.3 % less up-GEMM time, identical output;
+  // traced in one process.  The same for the down GEMM, two of its 8 blocks per wave,
+  // made it 0.6-1.5 % slower).  Buffer stores: rows at or past the tile's end get an
+  // offset past the buffer, which drops them without a branch.
+  u32x4_t pend[2][2];     // UP: the wave's row blocks 2 and 3 of the previous tile
+  int p_row0 = 0, p_col = 0, p_row_end = 0;     // nothing pending before the first tile
+  const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      out, static_cast<short>(0),
+      static_cast<int>(static_cast<uint32_t>(out_rows) * static_cast<uint32_t>(N_out) * 2u),
+      0x00020000);
+  auto store_pend = [&](int b) {
+    const int rbase = p_row0 + 32 * (b + 2) + (lane >> 2);
+    const int col = p_col + 8 * (lane & 3);
+    const bool c_ok = col < N_out;
+    const uint32_t o0 = rbase < p_row_end && c_ok
+                            ? static_cast<uint32_t>(rbase * N_out + col) * 2u : 0x80000000u;
+    const uint32_t o1 = rbase + 16 < p_row_end && c_ok
+                            ? static_cast<uint32_t>((rbase + 16) * N_out + col) * 2u : 0x80000000u;
+    __builtin_amdgcn_raw_buffer_store_b128(pend[b][0], out_rsrc, o0, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(pend[b][1], out_rsrc, o1, 0, 0);
+  };
 
   // The copies are buffer loads into LDS.  Input rows go through a resource of the
   // operand's size, and a copy that is skipped (wholly past the expert's last row) gets
@@ -722,9 +785,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
       }
     };
-    // one K step; FIRST: the tile's first, with no deferred MFMAs of a previous slice
-    auto step = [&](auto first_c, int kt) {
+    // one K step; FIRST: the tile's first, with no deferred MFMAs of a previous slice;
+    // PART 1: the step that stores the previous tile's pending blocks (UP)
+    auto step = [&](auto first_c, auto part_c, int kt) {
       constexpr bool FIRST = decltype(first_c)::value;
+      constexpr int PART = decltype(part_c)::value;
       // the slice after this one: the next K step, the next tile's first, or (after the
       // last step of this workgroup) this step's slice again into the idle ring slot,
       // so the issue below never branches and every source address stays in bounds
@@ -749,6 +814,10 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
 #pragma unroll
         for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
+        if constexpr (PART > 0) {
+          store_pend(0);
+          store_pend(1);
+        }
       } else {
         const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
         const uint16_t* Bs = As + TL_A_ELEMS;
@@ -784,16 +853,21 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
 #pragma unroll
             for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
           }
-          if (FIRST ? kk < 2 : kk < 1)
+          if (FIRST ? kk < 2 : kk < 1) {
             interleave_copies();
-          else
+          } else if (PART == 1 && kk == 2) {
+            store_pend(0);
+            store_pend(1);
+            interleave_copies();
+          } else {
             __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);
+          }
         }
       }
     };
-    step(std::true_type{}, 0);
+    step(std::true_type{}, std::integral_constant<int, UP ? 1 : 0>{}, 0);
     ++s;
-    for (int kt = 1; kt < nk; ++kt, ++s) step(std::false_type{}, kt);
+    for (int kt = 1; kt < nk; ++kt, ++s) step(std::false_type{}, std::integral_constant<int, 0>{}, kt);
     if constexpr (NB > 0) mfmas(1);     // the last slice's last sub-step
   };
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
@@ -821,8 +895,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       if (i < nb) {
         const int rb = t.row0 + 128 * wm + 32 * i;
         if (UP) {
-          store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out,
-                            s_stage[wave]);
+          if (i < 2)
+            store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out,
+                              s_stage[wave]);
+          else
+            stage_block<true>(acc[i][0], acc[i][1], s_stage[wave], pend[i - 2]);
         } else {
 #pragma unroll
           for (int j = 0; j < TL_NJ; ++j)
@@ -831,6 +908,15 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         }
       }
     }
+    if (UP) {
+      p_row0 = t.row0 + 128 * wm;
+      p_col = t.n0 + 32 * wn;
+      p_row_end = t.row_end;
+    }
+  }
+  if (UP) {     // the last tile's pending blocks
+    store_pend(0);
+    store_pend(1);
   }
   waitcnt_vm<0>();     // the last (unused) copy lands before the workgroup's LDS is released
 }
@@ -884,9 +970,10 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
 // pair capacity (the MFMAs, not the weight stream, bound such launches).
 // The tall kernel reads its input rows through a buffer resource with 32-bit byte
 // offsets, so its input operand must hold fewer than 2^30 elements.
-bool use_tall(int cap, int E, int x_rows, int K) {
+bool use_tall(int cap, int E, int x_rows, int K, int out_rows, int N) {
   return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS &&
-         static_cast<size_t>(x_rows) * static_cast<size_t>(K) < (size_t(1) << 30);
+         static_cast<size_t>(x_rows) * static_cast<size_t>(K) < (size_t(1) << 30) &&
+         static_cast<size_t>(out_rows) * static_cast<size_t>(N) < (size_t(1) << 30);
 }
 
 template <bool UP>
@@ -931,7 +1018,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
                      const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
                      void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, T, d))
+  if (use_tall(cap, E, T, d, cap, f))
     return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, wg, wu,
                                   static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
@@ -941,7 +1028,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
 int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
                        int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, cap, f))
+  if (use_tall(cap, E, cap, f, cap, d))
     return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E, wd, nullptr,
                                    static_cast<size_t>(d) * f, f, d, cap, cap, y_sorted, s);
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
