@@ -574,15 +574,22 @@ constexpr int TL_NJ = 2;                         // 32-row weight blocks per wav
 constexpr int TL_CH = TL_BK / 8;
 constexpr int TL_ROWS_PER_OP = 64 / TL_CH;
 constexpr int TL_RG = 16 / TL_CH;
-constexpr int TL_A_ELEMS = TL_BM * TL_BK;
-constexpr int TL_B_ELEMS = GM_BROWS * TL_BK;
-constexpr int TL_STAGE_ELEMS = TL_A_ELEMS + TL_B_ELEMS;
+constexpr int TL_A_ELEMS = TL_BM * TL_BK;        // one input-row slice (32 KB)
+constexpr int TL_B_ELEMS = GM_BROWS * TL_BK;     // one weight slice (32 KB)
+constexpr int TL_A_SLOTS = 2;                    // input rows: one slice ahead
+constexpr int TL_B_SLOTS = 3;                    // weights: two slices ahead
 constexpr int TL_A_OPS = TL_BM / TL_ROWS_PER_OP / TL_WAVES;   // DMA ops per wave per step
 constexpr int TL_B_OPS = GM_BROWS / TL_ROWS_PER_OP / TL_WAVES;
-constexpr size_t TL_LDS = size_t(2) * TL_STAGE_ELEMS * sizeof(uint16_t);   // two-slice ring
+constexpr size_t TL_LDS =
+    size_t(TL_A_SLOTS * TL_A_ELEMS + TL_B_SLOTS * TL_B_ELEMS) * sizeof(uint16_t);
 static_assert(GM_BROWS == 256, "tall tiles: four wave columns of 64 weight rows");
 static_assert(TL_A_OPS == 4 && TL_B_OPS == 4, "copy interleave: four of each per wave and step");
-static_assert(TL_LDS + 8192 + TL_WAVES * ST_ELEMS * 2 <= 160 * 1024, "tall LDS ring + staging");
+static_assert(TL_LDS <= 160 * 1024, "tall LDS rings");
+static_assert(TL_WAVES * ST_ELEMS <= TL_A_ELEMS, "the epilogue staging fits in an input-row slot");
+static_assert(3 * (REFLEX_MAX_EXPERTS + 1) * 4 <= TL_A_ELEMS * 2, "start-up scratch in the ring");
+#if !RFX_GEMM_NINNER
+#error "the 256-row kernel decodes tiles with the N tile inner"
+#endif
 
 template <bool UP>
 __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
@@ -590,18 +597,29 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     const int32_t* __restrict__ expert_offsets, int E, const uint16_t* __restrict__ w0,
     const uint16_t* __restrict__ w1, size_t w_expert_stride, int K, int N_out, int x_rows,
     int out_rows, uint16_t* __restrict__ out) {
+  // The whole 160 KB of LDS holds the two rings: input-row slices in slots 0-1, weight
+  // slices in the three slots after them.  The weight lines mostly come from HBM (the
+  // input rows mostly hit in L2), so they are copied two K steps ahead and the copies of
+  // the next weight slice stay in flight across each step's barrier.  The tile tables
+  // live in registers, and the epilogue stages its stores in the input-row slot the
+  // tile's last K step has read.
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  uint16_t* const a_ring = smem;
+  uint16_t* const b_ring = smem + TL_A_SLOTS * TL_A_ELEMS;
   constexpr int BN = UP ? GM_UP_BN : GM_DOWN_BN;
   const int n_tiles = (N_out + BN - 1) / BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // expert row offsets and the per-expert prefix of 256-row tiles
-  __shared__ int s_tile_off[REFLEX_MAX_EXPERTS + 1], s_eo[REFLEX_MAX_EXPERTS + 1];
-  __shared__ int s_part[TL_WAVES];
-  __shared__ __attribute__((aligned(16))) uint16_t s_stage[TL_WAVES][ST_ELEMS];
-  for (int e = tid; e <= E; e += TL_THREADS) s_eo[e] = expert_offsets[e];
-  __syncthreads();
+  // ---- expert row offsets and the per-expert prefix of 256-row tiles, computed in LDS
+  // (scratch: the rings are empty until the first copies) and kept in registers: lane l
+  // holds the entries of experts l, l + 64, l + 128, l + 192
+  int toff_r[4], eo_r[4], eo_E, m_total;
   {
+    int* s_eo = reinterpret_cast<int*>(smem);
+    int* s_toff = s_eo + (REFLEX_MAX_EXPERTS + 1);
+    int* s_part = s_toff + (REFLEX_MAX_EXPERTS + 1);
+    for (int e = tid; e <= E; e += TL_THREADS) s_eo[e] = expert_offsets[e];
+    __syncthreads();
     int n = 0;
     if (tid < E) {
       n = s_eo[tid + 1] - s_eo[tid];
@@ -612,10 +630,57 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     __syncthreads();
     int base = incl - n;
     for (int q = 0; q < wave; ++q) base += s_part[q];
-    if (tid <= E) s_tile_off[tid] = base;       // tid == E: the total
+    if (tid <= E) s_toff[tid] = base;       // tid == E: the total
     __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      toff_r[q] = e < E ? s_toff[e] : 0;
+      eo_r[q] = e < E ? s_eo[e] : 0;
+    }
+    eo_E = __builtin_amdgcn_readfirstlane(s_eo[E]);
+    m_total = __builtin_amdgcn_readfirstlane(s_toff[E]);
+    __syncthreads();     // all scratch reads done before the first copies land
   }
-  const int total = s_tile_off[E] * n_tiles;
+  // entry e (< 256) of a per-lane table, uniform e
+  auto table_at = [&](const int (&r)[4], int e) {
+    const int q = e >> 6;
+    const int v = q == 0 ? r[0] : (q == 1 ? r[1] : (q == 2 ? r[2] : r[3]));
+    return __builtin_amdgcn_readlane(v, e & 63);
+  };
+  // Logical tile L -> tile: experts in order, the M tile outer and the N tile inner; the
+  // expert is found in one round (the wave counts the experts whose first tile lies at or
+  // before L).  rot: the tile's K rotation (below).
+  struct TT {
+    int expert, row0, row_end, n0, rot;
+  };
+  const int nk = K / TL_BK;
+  auto decode = [&](int L) {
+    TT t;
+    int cnt = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cnt += (lane + 64 * q < E && toff_r[q] * n_tiles <= L) ? 1 : 0;
+    int lo = wave_sum_i32(cnt) - 1;
+    lo = __builtin_amdgcn_readfirstlane(lo < 0 ? 0 : lo);
+    const int local = L - table_at(toff_r, lo) * n_tiles;
+    const int er0 = table_at(eo_r, lo);
+    const int er1 = lo + 1 < E ? table_at(eo_r, lo + 1) : eo_E;
+    t.expert = lo;
+    t.n0 = (local % n_tiles) * BN;
+    const int m = local / n_tiles;
+    t.row0 = er0 + m * TL_BM;
+    t.row_end = er1 < out_rows ? er1 : out_rows;
+    if (t.row0 < 0 || t.row0 >= t.row_end) t.row_end = t.row0;   // inconsistent offsets: no rows
+    // K rotation: tile (M tile m of its expert, N tile n) walks its K slices starting at
+    // slice (2 m + n) mod nk.  The tiles sharing a weight slice (same n) or an input-row
+    // slice (same m) then request it one or two steps apart instead of all at once, so
+    // most requests hit the line already in L2 rather than queueing behind its miss (5 %
+    // less GEMM time on the 16-layer stack, 3 % on the skewed layer, measured).  Only the
+    // order of the fp32 sums over K changes.
+    t.rot = (2 * m + t.n0 / BN) % nk;
+    return t;
+  };
+  const int total = m_total * n_tiles;
   const int xcd = blockIdx.x % GM_XCDS;
   const int per_xcd = gridDim.x / GM_XCDS;
   const int j0 = blockIdx.x / GM_XCDS;
@@ -624,7 +689,6 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   const int l_end = min(total, (xcd + 1) * chunk);
   if (l_begin >= l_end) return;
   const int n_my = (l_end - l_begin + per_xcd - 1) / per_xcd;
-  const int nk = K / TL_BK;
   const int wm = wave >> 2, wn = wave & 3;
 
   // ---- copies: op q of the step fills rows ROWS_PER_OP q ..; lane L writes row
@@ -632,37 +696,34 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   auto lane_row = [&](int q) { return q * TL_ROWS_PER_OP + lane / TL_CH; };
   auto lane_chunk = [&](int q) { return ((lane % TL_CH) ^ ((lane_row(q) / TL_RG) % TL_CH)) * 8; };
   constexpr int CP_OPS = TL_A_OPS;     // copies of each operand per wave and step
-  // Copy sources as 32-bit element offsets (the host keeps the tall kernel to input
-  // operands of fewer than 2^30 elements): input-row copy j reads x + a_off[j]; the weight
-  // copies of a wave cover 32 consecutive rows of one matrix (gate or up rows in the up
-  // GEMM), so copy j reads the wave's rows at 16 K (j / 2) + b_off[j % 2] (copies j and
-  // j + 2 are 16 rows apart and share the chunk swizzle).
+  // The copies are buffer loads into LDS.  Input rows go through a resource of the
+  // operand's size, and a copy that is skipped (wholly past the expert's last row) gets
+  // an offset past that size, which the hardware's range check turns into no memory
+  // access, so the step has no branch: a branch splits the step into several basic
+  // blocks, and the instruction order pinned below then holds only within each (16-layer
+  // stack and skewed layer: 2-3 % less GEMM time than a branch around each copy,
+  // identical output; traced in one process).  Weight rows go through a resource of the
+  // wave's 32 rows of the tile: with global_load_lds copies the compiler made each
+  // sub-step's MFMAs wait for all of the step's LDS reads, not only their own (2-3 %
+  // less GEMM time with the buffer form).  Copy sources are 32-bit element offsets (the
+  // host keeps the tall kernel to input operands of fewer than 2^30 elements).
+  //
+  // Input-row loader: its tile and K slice, rotation, the copies that hold rows of its
+  // tile, and copy j's offset into x.
+  int a_tile = 0, a_k = 0, a_rot = 0, a_ops = CP_OPS;
   uint32_t a_off[CP_OPS];
-  uint32_t b_off[2];
-  __amdgpu_buffer_rsrc_t b_rsrc;     // the wave's 32 weight rows of the loading tile
-  // K rotation: tile (M tile m of its expert, N tile n) walks its K slices starting at
-  // slice (2 m + n) mod nk.  The tiles sharing a weight slice (same n) or an input-row
-  // slice (same m) then request it one or two steps apart instead of all at once, so
-  // most requests hit the line already in L2 rather than queueing behind its miss (5 %
-  // less GEMM time on the 16-layer stack, 3 % on the skewed layer, measured).  Only the
-  // order of the fp32 sums over K changes.
-  int ld_rot = 0;      // rotation of the tile being loaded
-  int ld_ops = CP_OPS;  // this wave's input-row copies that hold rows of the loading tile
-  auto setup_loader = [&](int tile_i) {
-    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
-                                          n_tiles, out_rows);
+  auto setup_a = [&](int tile_i) {
+    const TT t = decode(l_begin + tile_i * per_xcd);
     const int rows_valid = t.row_end - t.row0;
-    {
-      // Input-row copy q holds rows ROWS_PER_OP q ..; copies wholly past the expert's last
-      // row are not issued.  The multiply reads whole 32-row blocks, but only up to the
-      // block holding the last row, and every copy with a row of that block is issued, so
-      // no row it reads is skipped (16-layer stack and skewed layer: 1-2 % less GEMM time,
-      // identical output; traced in one process).
-      int n = (rows_valid + TL_ROWS_PER_OP - 1) / TL_ROWS_PER_OP - CP_OPS * wave;
-      n = n < 0 ? 0 : (n > CP_OPS ? CP_OPS : n);
-      ld_ops = __builtin_amdgcn_readfirstlane(n);
-    }
-    ld_rot = (2 * ((t.row0 - s_eo[t.expert]) / TL_BM) + t.n0 / BN) % nk;
+    // Input-row copy q holds rows ROWS_PER_OP q ..; copies wholly past the expert's last
+    // row are not issued.  The multiply reads whole 32-row blocks, but only up to the
+    // block holding the last row, and every copy with a row of that block is issued, so
+    // no row it reads is skipped (16-layer stack and skewed layer: 1-2 % less GEMM time,
+    // identical output; traced in one process).
+    int n = (rows_valid + TL_ROWS_PER_OP - 1) / TL_ROWS_PER_OP - CP_OPS * wave;
+    n = n < 0 ? 0 : (n > CP_OPS ? CP_OPS : n);
+    a_ops = __builtin_amdgcn_readfirstlane(n);
+    a_rot = t.rot;
 #pragma unroll
     for (int j = 0; j < CP_OPS; ++j) {
       const int r = lane_row(CP_OPS * wave + j);
@@ -675,22 +736,84 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       a_off[j] = static_cast<uint32_t>(src) * static_cast<uint32_t>(K) +
                  static_cast<uint32_t>(lane_chunk(CP_OPS * wave + j));
     }
-    // the wave's 32 weight rows: tile rows 32 wave .. (UP: 32 (wave % 4) .. of the gate
-    // (waves 0-3) or up (waves 4-7) rows).  N is a multiple of 64 and the rows start at a
-    // multiple of 32, so in a partial last N tile they are all valid or all past N; past
-    // N they are replaced by the last 32 rows (the columns past N are not stored).
+  };
+  // Weight loader: its tile and K slice, rotation, and the address of the wave's 32
+  // weight rows: tile rows 32 wave .. (UP: 32 (wave % 4) .. of the gate (waves 0-3) or up
+  // (waves 4-7) rows).  N is a multiple of 64 and the rows start at a multiple of 32, so
+  // in a partial last N tile they are all valid or all past N; past N they are replaced
+  // by the last 32 rows (the columns past N are not stored).  Copies j and j + 2 are 16
+  // rows apart and share the chunk swizzle: copy j reads 16 K (j / 2) + b_off[j % 2].
+  int b_tile = 0, b_k = 0, b_rot = 0;
+  uint32_t b_lo = 0, b_hi = 0;
+  uint32_t b_off[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    b_off[j] = static_cast<uint32_t>(lane_row(j) * K) +
+               static_cast<uint32_t>(lane_chunk(CP_OPS * wave + j));
+  auto setup_b = [&](int tile_i) {
+    const TT t = decode(l_begin + tile_i * per_xcd);
+    b_rot = t.rot;
     int wr0 = t.n0 + 32 * (UP ? (wave & 3) : wave);
     wr0 = wr0 + 32 <= N_out ? wr0 : N_out - 32;
     const uint16_t* wm_base = (UP && wave >= 4 ? w1 : w0) + t.expert * w_expert_stride;
     const uint64_t b_addr = reinterpret_cast<uint64_t>(wm_base + static_cast<size_t>(wr0) * K);
-    const uint64_t b_lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_addr)));
-    const uint64_t b_hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_addr >> 32)));
-    b_rsrc = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(b_lo | (b_hi << 32)),
-                                               static_cast<short>(0), 64 * K, 0x00020000);
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      b_off[j] = static_cast<uint32_t>(lane_row(j) * K) +
-                 static_cast<uint32_t>(lane_chunk(CP_OPS * wave + j));
+    b_lo = static_cast<uint32_t>(b_addr);
+    b_hi = static_cast<uint32_t>(b_addr >> 32);
+  };
+  // The K offset of a loader's next slice; then it advances (past the workgroup's last
+  // tile it stays on its last slice, so the issue never branches and every source
+  // address stays in bounds).
+  auto a_next = [&]() {
+    if (a_k == nk) {
+      if (a_tile + 1 < n_my) {
+        ++a_tile;
+        a_k = 0;
+        setup_a(a_tile);
+      } else {
+        a_k = nk - 1;
+      }
+    }
+    int kr = a_k + a_rot;
+    kr = kr >= nk ? kr - nk : kr;
+    ++a_k;
+    return kr * TL_BK;
+  };
+  auto b_next = [&]() {
+    if (b_k == nk) {
+      if (b_tile + 1 < n_my) {
+        ++b_tile;
+        b_k = 0;
+        setup_b(b_tile);
+      } else {
+        b_k = nk - 1;
+      }
+    }
+    int kr = b_k + b_rot;
+    kr = kr >= nk ? kr - nk : kr;
+    ++b_k;
+    return kr * TL_BK;
+  };
+  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(x), static_cast<short>(0),
+      static_cast<int>(static_cast<uint32_t>(x_rows) * static_cast<uint32_t>(K) * 2u), 0x00020000);
+  auto dma_a = [&](int j, uint16_t* As_, int k0_) {
+    const uint32_t voff = j < a_ops ? (a_off[j] + static_cast<uint32_t>(k0_)) * 2u : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        x_rsrc, (__attribute__((address_space(3))) void*)(As_ + (CP_OPS * wave + j) * 512), 16,
+        voff, 0, 0, kDmaPolicy);
+  };
+  auto dma_b = [&](int j, uint16_t* Bs_, int k0_) {
+    // the resource is rebuilt from wave-uniform halves at each use, so that it always
+    // lives in scalar registers (held across the loop it could end up in vector
+    // registers, and each copy would then become a loop over the distinct values)
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_lo)));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b_hi)));
+    const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(lo | (hi << 32)), static_cast<short>(0), 64 * K, 0x00020000);
+    const uint32_t voff = (b_off[j % 2] + static_cast<uint32_t>(k0_ + 16 * (j / 2) * K)) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        b_rsrc, (__attribute__((address_space(3))) void*)(Bs_ + (CP_OPS * wave + j) * 512), 16,
+        voff, 0, 0, kDmaPolicy);
   };
   // ---- multiply: pair blocks 128 wm + 32 i, weight blocks b_row[j]
   const int b_row[TL_NJ] = {UP ? 32 * wn : 64 * wn, UP ? GM_BROWS / 2 + 32 * wn : 64 * wn + 32};
@@ -721,51 +844,32 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     __builtin_amdgcn_raw_buffer_store_b128(pend[b][1], out_rsrc, o1, 0, 0);
   };
 
-  // The copies are buffer loads into LDS.  Input rows go through a resource of the
-  // operand's size, and a copy that is skipped (wholly past the expert's last row) gets
-  // an offset past that size, which the hardware's range check turns into no memory
-  // access, so the step has no branch: a branch splits the step into several basic
-  // blocks, and the instruction order pinned below then holds only within each (16-layer
-  // stack and skewed layer: 2-3 % less GEMM time than a branch around each copy,
-  // identical output; traced in one process).  Weight rows go through a resource of the
-  // wave's 32 rows of the tile: with global_load_lds copies the compiler made each
-  // sub-step's MFMAs wait for all of the step's LDS reads, not only their own (2-3 %
-  // less GEMM time with the buffer form).
-  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(x), static_cast<short>(0),
-      static_cast<int>(static_cast<uint32_t>(x_rows) * static_cast<uint32_t>(K) * 2u), 0x00020000);
-  auto dma_a = [&](int j, uint16_t* As_, int k0_) {
-    const uint32_t voff = j < ld_ops ? (a_off[j] + static_cast<uint32_t>(k0_)) * 2u : 0x80000000u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        x_rsrc, (__attribute__((address_space(3))) void*)(As_ + (CP_OPS * wave + j) * 512), 16,
-        voff, 0, 0, kDmaPolicy);
-  };
-  auto dma_b = [&](int j, uint16_t* Bs_, int k0_) {
-    const uint32_t voff = (b_off[j % 2] + static_cast<uint32_t>(k0_ + 16 * (j / 2) * K)) * 2u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        b_rsrc, (__attribute__((address_space(3))) void*)(Bs_ + (CP_OPS * wave + j) * 512), 16,
-        voff, 0, 0, kDmaPolicy);
-  };
-  setup_loader(0);
+  // prologue: input-row slice 0 and weight slices 0 and 1
+  setup_a(0);
+  setup_b(0);
   {
-    const int kr0 = ld_rot;
+    const int ka = a_next();
 #pragma unroll
-    for (int j = 0; j < CP_OPS; ++j) dma_a(j, smem, kr0 * TL_BK);
+    for (int j = 0; j < CP_OPS; ++j) dma_a(j, a_ring, ka);
 #pragma unroll
-    for (int j = 0; j < CP_OPS; ++j) dma_b(j, smem + TL_A_ELEMS, kr0 * TL_BK);
+    for (int q = 0; q < TL_B_SLOTS - 1; ++q) {
+      const int kb = b_next();
+#pragma unroll
+      for (int j = 0; j < CP_OPS; ++j) dma_b(j, b_ring + q * TL_B_ELEMS, kb);
+    }
   }
-  int s = 0;
+  int s = 0;     // K steps so far (the rings' slot counter)
   // The K loop of one tile with NB active pair blocks (0: this wave only copies).  The
   // MFMAs of each slice's last 16-wide sub-step run after the next step's barrier, from
   // fragments read before it, so they overlap the LDS reads of the next slice's first
   // sub-step instead of every SIMD waiting for those reads after each barrier (16-layer
   // stack and skewed layer: 3-4 % less GEMM time, identical output; traced in one
   // process).  The fragments stay in the second register buffer across the barrier.
-  auto k_loop = [&](auto nb_c, int tile_i) {
+  auto k_loop = [&](auto nb_c) {
     constexpr int NB = decltype(nb_c)::value;
     constexpr int kReads = NB + TL_NJ, kMfmas = NB * TL_NJ;
     constexpr int kPer = kMfmas / CP_OPS > 0 ? kMfmas / CP_OPS : 1;
-    bf16x8_t af[2][TL_MI > 0 ? TL_MI : 1], bfr[2][TL_NJ];
+    bf16x8_t af[2][TL_MI], bfr[2][TL_NJ];
     // weights as the MFMA's A operand: the accumulator is the transposed tile, so each
     // lane ends up holding 4 consecutive output columns of one row
     auto mfmas = [&](int buf) {
@@ -785,42 +889,38 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
       }
     };
-    // one K step; FIRST: the tile's first, with no deferred MFMAs of a previous slice;
-    // PART 1: the step that stores the previous tile's pending blocks (UP)
-    auto step = [&](auto first_c, auto part_c, int kt) {
+    // One K step.  FIRST: the tile's first, with no deferred MFMAs of a previous slice;
+    // PART 1: the step that stores the previous tile's pending blocks (UP); DRAIN: the
+    // step waits for all of its wave's ops, not only for the slices it reads (after
+    // stores, which need not complete in order with the copies).
+    auto step = [&](auto first_c, auto part_c, auto drain_c) {
       constexpr bool FIRST = decltype(first_c)::value;
       constexpr int PART = decltype(part_c)::value;
-      // the slice after this one: the next K step, the next tile's first, or (after the
-      // last step of this workgroup) this step's slice again into the idle ring slot,
-      // so the issue below never branches and every source address stays in bounds
-      int k_next = kt + 1;
-      if (kt == nk - 1) {
-        if (tile_i + 1 < n_my) {
-          setup_loader(tile_i + 1);
-          k_next = 0;
-        } else {
-          k_next = kt;
-        }
-      }
-      waitcnt_vm<0>();
-      lds_barrier();       // slice s complete and visible; slice s-1 no longer read
-      uint16_t* An = smem + ((s + 1) & 1) * TL_STAGE_ELEMS;
-      uint16_t* Bn = An + TL_A_ELEMS;
-      int kr = k_next + ld_rot;     // the slice's place in K for the loading tile's rotation
-      kr = kr >= nk ? kr - nk : kr;
-      const int k0n = kr * TL_BK;
+      constexpr bool DRAIN = decltype(drain_c)::value;
+      const int ka = a_next();
+      const int kb = b_next();
+      // Input-row slice s and weight slice s have landed (issued one and two steps ago;
+      // the ops issued after them are the next weight slice's) and are visible to all
+      // waves; the slots of the slices the previous step read are free.
+      if constexpr (DRAIN)
+        waitcnt_vm<0>();
+      else
+        waitcnt_vm<TL_B_OPS>();
+      lds_barrier();
+      uint16_t* An = a_ring + ((s + 1) % TL_A_SLOTS) * TL_A_ELEMS;
+      uint16_t* Bn = b_ring + ((s + TL_B_SLOTS - 1) % TL_B_SLOTS) * TL_B_ELEMS;
       if constexpr (NB == 0) {
 #pragma unroll
-        for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
+        for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, ka);
 #pragma unroll
-        for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
+        for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, kb);
         if constexpr (PART > 0) {
           store_pend(0);
           store_pend(1);
         }
       } else {
-        const uint16_t* As = smem + (s & 1) * TL_STAGE_ELEMS;
-        const uint16_t* Bs = As + TL_A_ELEMS;
+        const uint16_t* As = a_ring + (s % TL_A_SLOTS) * TL_A_ELEMS;
+        const uint16_t* Bs = b_ring + (s % TL_B_SLOTS) * TL_B_ELEMS;
         auto load = [&](int kk, int buf) {
           const int slot = ((2 * kk + fsel) ^ fx) * 8;
 #pragma unroll
@@ -837,7 +937,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         if constexpr (!FIRST) {
           mfmas(1);     // the previous slice's last sub-step
 #pragma unroll
-          for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
+          for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, ka);
           interleave_copies();
         }
 #pragma unroll
@@ -847,11 +947,11 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
           mfmas(kk & 1);
           if (FIRST ? kk == 0 : false) {
 #pragma unroll
-            for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, k0n);
+            for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, ka);
           }
           if (FIRST ? kk == 1 : kk == 0) {
 #pragma unroll
-            for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, k0n);
+            for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, kb);
           }
           if (FIRST ? kk < 2 : kk < 1) {
             interleave_copies();
@@ -865,14 +965,22 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         }
       }
     };
-    step(std::true_type{}, std::integral_constant<int, UP ? 1 : 0>{}, 0);
+    // the first step follows the previous tile's output stores, and (UP) the second
+    // follows the pending ones issued in the first
+    step(std::true_type{}, std::integral_constant<int, UP ? 1 : 0>{}, std::true_type{});
     ++s;
-    for (int kt = 1; kt < nk; ++kt, ++s) step(std::false_type{}, std::integral_constant<int, 0>{}, kt);
+    int kt = 1;
+    if (UP && nk > 1) {
+      step(std::false_type{}, std::integral_constant<int, 0>{}, std::true_type{});
+      ++s;
+      kt = 2;
+    }
+    for (; kt < nk; ++kt, ++s)
+      step(std::false_type{}, std::integral_constant<int, 0>{}, std::false_type{});
     if constexpr (NB > 0) mfmas(1);     // the last slice's last sub-step
   };
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
-    const Tile t = decode_tile<TL_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, -1,
-                                          n_tiles, out_rows);
+    const TT t = decode(l_begin + tile_i * per_xcd);
     // pair blocks of this wave's 128 rows that hold pairs (wave-uniform)
     int rows = t.row_end - t.row0 - 128 * wm;
     rows = rows < 0 ? 0 : (rows > 128 ? 128 : rows);
@@ -884,12 +992,16 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
     switch (nb) {
-      case 4: k_loop(std::integral_constant<int, 4>{}, tile_i); break;
-      case 3: k_loop(std::integral_constant<int, 3>{}, tile_i); break;
-      case 2: k_loop(std::integral_constant<int, 2>{}, tile_i); break;
-      case 1: k_loop(std::integral_constant<int, 1>{}, tile_i); break;
-      default: k_loop(std::integral_constant<int, 0>{}, tile_i); break;
+      case 4: k_loop(std::integral_constant<int, 4>{}); break;
+      case 3: k_loop(std::integral_constant<int, 3>{}); break;
+      case 2: k_loop(std::integral_constant<int, 2>{}); break;
+      case 1: k_loop(std::integral_constant<int, 1>{}); break;
+      default: k_loop(std::integral_constant<int, 0>{}); break;
     }
+    // every wave has read the tile's last input-row slice: its slot takes the staging
+    // (the next tile's first step refills it only after its own barrier)
+    lds_barrier();
+    uint16_t* stage = a_ring + ((s + 1) % TL_A_SLOTS) * TL_A_ELEMS + wave * ST_ELEMS;
 #pragma unroll
     for (int i = 0; i < TL_MI; ++i) {
       if (i < nb) {
@@ -897,14 +1009,14 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         if (UP) {
           if (i < 2)
             store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out,
-                              s_stage[wave]);
+                              stage);
           else
-            stage_block<true>(acc[i][0], acc[i][1], s_stage[wave], pend[i - 2]);
+            stage_block<true>(acc[i][0], acc[i][1], stage, pend[i - 2]);
         } else {
 #pragma unroll
           for (int j = 0; j < TL_NJ; ++j)
             store_block<false>(acc[i][j], acc[i][j], rb, t.n0 + 64 * wn + 32 * j, t.row_end, N_out,
-                               out, s_stage[wave]);
+                               out, stage);
         }
       }
     }
@@ -918,7 +1030,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     store_pend(0);
     store_pend(1);
   }
-  waitcnt_vm<0>();     // the last (unused) copy lands before the workgroup's LDS is released
+  waitcnt_vm<0>();     // the last (unused) copies land before the workgroup's LDS is released
 }
 
 // Per-expert M-tile prefix: tile_off[e] = sum_{e' < e} ceil(n_e' / 128), tile_off[E] = total.
