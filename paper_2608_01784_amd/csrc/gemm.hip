@@ -311,45 +311,6 @@ __device__ __forceinline__ void store_block(const f32x16_t& g, const f32x16_t& u
 }
 
 
-// The staging half of store_block for the 256-row kernel: one 32 x 32 block (UP: SiLU(g)
-// u) through the wave's staging buffer into r, rows l/4 and 16 + l/4, columns 8 (l%4)
-// ..+7 of the block, for stores issued later.
-template <bool UP>
-__device__ __forceinline__ void stage_block(const f32x16_t& g, const f32x16_t& u, uint16_t* stage,
-                                            u32x4_t (&r)[2]) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(stage));
-  const uint32_t wr = base + ((lane & 31) * ST_LD + 4 * (lane >> 5)) * 2;
-  const uint32_t rd = base + ((lane >> 2) * ST_LD + 8 * (lane & 3)) * 2;
-  u32x2_t v[4];
-#pragma unroll
-  for (int gi = 0; gi < 4; ++gi) {
-    float a4[4];
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      if (UP) {
-        const float gg = g[4 * gi + h], uu = u[4 * gi + h];
-        const float en = __builtin_amdgcn_exp2f(gg * -1.4426950408889634f);
-        a4[h] = gg * __builtin_amdgcn_rcpf(1.0f + en) * uu;
-      } else {
-        a4[h] = g[4 * gi + h];
-      }
-    }
-    v[gi] = u32x2_t{pack_bf16x2(a4[0], a4[1]), pack_bf16x2(a4[2], a4[3])};
-  }
-  asm volatile(
-      "ds_write_b64 %2, %4\n\t"
-      "ds_write_b64 %2, %5 offset:16\n\t"
-      "ds_write_b64 %2, %6 offset:32\n\t"
-      "ds_write_b64 %2, %7 offset:48\n\t"
-      "ds_read_b128 %0, %3\n\t"
-      "ds_read_b128 %1, %3 offset:1280\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1])
-      : "v"(wr), "v"(rd), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3])
-      : "memory");
-}
-
 // UP = true : act = SiLU(X Wg^T) * (X Wu^T);  UP = false: y = act Wd^T.
 template <bool UP>
 __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
@@ -819,31 +780,6 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
   const int b_row[TL_NJ] = {UP ? 32 * wn : 64 * wn, UP ? GM_BROWS / 2 + 32 * wn : 64 * wn + 32};
   const int frow = lane & 31, fsel = lane >> 5, fx = (frow / TL_RG) % TL_CH;
   f32x16_t acc[TL_MI][TL_NJ];
-  // UP: half of each wave's output (row blocks 2 and 3 of its 4), staged in row layout at
-  // the tile's end, is stored during the next tile's first K step, between its MFMAs,
-  // instead of in the burst in which all workgroups store at once and no MFMAs run
-  // (16-layer stack and skewed layer: 1.0-1.3 % less up-GEMM time, identical output;
-  // traced in one process.  The same for the down GEMM, two of its 8 blocks per wave,
-  // made it 0.6-1.5 % slower).  Buffer stores: rows at or past the tile's end get an
-  // offset past the buffer, which drops them without a branch.
-  u32x4_t pend[2][2];     // UP: the wave's row blocks 2 and 3 of the previous tile
-  int p_row0 = 0, p_col = 0, p_row_end = 0;     // nothing pending before the first tile
-  const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      out, static_cast<short>(0),
-      static_cast<int>(static_cast<uint32_t>(out_rows) * static_cast<uint32_t>(N_out) * 2u),
-      0x00020000);
-  auto store_pend = [&](int b) {
-    const int rbase = p_row0 + 32 * (b + 2) + (lane >> 2);
-    const int col = p_col + 8 * (lane & 3);
-    const bool c_ok = col < N_out;
-    const uint32_t o0 = rbase < p_row_end && c_ok
-                            ? static_cast<uint32_t>(rbase * N_out + col) * 2u : 0x80000000u;
-    const uint32_t o1 = rbase + 16 < p_row_end && c_ok
-                            ? static_cast<uint32_t>((rbase + 16) * N_out + col) * 2u : 0x80000000u;
-    __builtin_amdgcn_raw_buffer_store_b128(pend[b][0], out_rsrc, o0, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b128(pend[b][1], out_rsrc, o1, 0, 0);
-  };
-
   // prologue: input-row slice 0 and weight slices 0 and 1
   setup_a(0);
   setup_b(0);
@@ -890,19 +826,16 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       }
     };
     // One K step.  FIRST: the tile's first, with no deferred MFMAs of a previous slice;
-    // PART 1: the step that stores the previous tile's pending blocks (UP); DRAIN: the
-    // step waits for all of its wave's ops, not only for the slices it reads (after
-    // stores, which need not complete in order with the copies).
-    auto step = [&](auto first_c, auto part_c, auto drain_c) {
+    // it follows the previous tile's output stores, which need not complete in order with
+    // the copies, so it waits for all of its wave's ops.
+    auto step = [&](auto first_c) {
       constexpr bool FIRST = decltype(first_c)::value;
-      constexpr int PART = decltype(part_c)::value;
-      constexpr bool DRAIN = decltype(drain_c)::value;
       const int ka = a_next();
       const int kb = b_next();
       // Input-row slice s and weight slice s have landed (issued one and two steps ago;
       // the ops issued after them are the next weight slice's) and are visible to all
       // waves; the slots of the slices the previous step read are free.
-      if constexpr (DRAIN)
+      if constexpr (FIRST)
         waitcnt_vm<0>();
       else
         waitcnt_vm<TL_B_OPS>();
@@ -914,10 +847,6 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         for (int j = 0; j < CP_OPS; ++j) dma_a(j, An, ka);
 #pragma unroll
         for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, kb);
-        if constexpr (PART > 0) {
-          store_pend(0);
-          store_pend(1);
-        }
       } else {
         const uint16_t* As = a_ring + (s % TL_A_SLOTS) * TL_A_ELEMS;
         const uint16_t* Bs = b_ring + (s % TL_B_SLOTS) * TL_B_ELEMS;
@@ -953,30 +882,16 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
 #pragma unroll
             for (int j = 0; j < CP_OPS; ++j) dma_b(j, Bn, kb);
           }
-          if (FIRST ? kk < 2 : kk < 1) {
+          if (FIRST ? kk < 2 : kk < 1)
             interleave_copies();
-          } else if (PART == 1 && kk == 2) {
-            store_pend(0);
-            store_pend(1);
-            interleave_copies();
-          } else {
+          else
             __builtin_amdgcn_sched_group_barrier(0x008, kMfmas, 0);
-          }
         }
       }
     };
-    // the first step follows the previous tile's output stores, and (UP) the second
-    // follows the pending ones issued in the first
-    step(std::true_type{}, std::integral_constant<int, UP ? 1 : 0>{}, std::true_type{});
+    step(std::true_type{});
     ++s;
-    int kt = 1;
-    if (UP && nk > 1) {
-      step(std::false_type{}, std::integral_constant<int, 0>{}, std::true_type{});
-      ++s;
-      kt = 2;
-    }
-    for (; kt < nk; ++kt, ++s)
-      step(std::false_type{}, std::integral_constant<int, 0>{}, std::false_type{});
+    for (int kt = 1; kt < nk; ++kt, ++s) step(std::false_type{});
     if constexpr (NB > 0) mfmas(1);     // the last slice's last sub-step
   };
   for (int tile_i = 0; tile_i < n_my; ++tile_i) {
@@ -1007,11 +922,7 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
       if (i < nb) {
         const int rb = t.row0 + 128 * wm + 32 * i;
         if (UP) {
-          if (i < 2)
-            store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out,
-                              stage);
-          else
-            stage_block<true>(acc[i][0], acc[i][1], stage, pend[i - 2]);
+          store_block<true>(acc[i][0], acc[i][1], rb, t.n0 + 32 * wn, t.row_end, N_out, out, stage);
         } else {
 #pragma unroll
           for (int j = 0; j < TL_NJ; ++j)
@@ -1020,15 +931,6 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
         }
       }
     }
-    if (UP) {
-      p_row0 = t.row0 + 128 * wm;
-      p_col = t.n0 + 32 * wn;
-      p_row_end = t.row_end;
-    }
-  }
-  if (UP) {     // the last tile's pending blocks
-    store_pend(0);
-    store_pend(1);
   }
   waitcnt_vm<0>();     // the last (unused) copies land before the workgroup's LDS is released
 }
@@ -1082,10 +984,9 @@ int launch_gemm(const uint16_t* x, const int32_t* gather, const int32_t* tile_of
 // pair capacity (the MFMAs, not the weight stream, bound such launches).
 // The tall kernel reads its input rows through a buffer resource with 32-bit byte
 // offsets, so its input operand must hold fewer than 2^30 elements.
-bool use_tall(int cap, int E, int x_rows, int K, int out_rows, int N) {
+bool use_tall(int cap, int E, int x_rows, int K) {
   return RFX_TALL_MIN_ROWS > 0 && E > 0 && cap / E >= RFX_TALL_MIN_ROWS &&
-         static_cast<size_t>(x_rows) * static_cast<size_t>(K) < (size_t(1) << 30) &&
-         static_cast<size_t>(out_rows) * static_cast<size_t>(N) < (size_t(1) << 30);
+         static_cast<size_t>(x_rows) * static_cast<size_t>(K) < (size_t(1) << 30);
 }
 
 template <bool UP>
@@ -1130,7 +1031,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
                      const uint16_t* wg, const uint16_t* wu, int T, int E, int d, int f, int cap,
                      void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, T, d, cap, f))
+  if (use_tall(cap, E, T, d))
     return launch_gemm_tall<true>(h, sorted_token, expert_offsets, E, wg, wu,
                                   static_cast<size_t>(f) * d, d, f, T, cap, routed_act(ws, E), s);
   return launch_gemm<true>(h, sorted_token, static_cast<const int32_t*>(ws), expert_offsets, E, -1,
@@ -1140,7 +1041,7 @@ int launch_swiglu_up(const uint16_t* h, const int32_t* sorted_token, const int32
 int launch_swiglu_down(const int32_t* expert_offsets, const uint16_t* wd, int E, int d, int f,
                        int cap, uint16_t* y_sorted, void* ws, hipStream_t s) {
   if (cap <= 0) return REFLEX_OK;
-  if (use_tall(cap, E, cap, f, cap, d))
+  if (use_tall(cap, E, cap, f))
     return launch_gemm_tall<false>(routed_act(ws, E), nullptr, expert_offsets, E, wd, nullptr,
                                    static_cast<size_t>(d) * f, f, d, cap, cap, y_sorted, s);
   return launch_gemm<false>(routed_act(ws, E), nullptr, static_cast<const int32_t*>(ws),
