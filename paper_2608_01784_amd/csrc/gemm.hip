@@ -9,7 +9,9 @@
 // (tile_off) cuts each expert's rows into 128-row M tiles, so no launch shape
 // depends on the device-resident per-expert counts.
 //
-// Tile 128 (M) x GM_BROWS (256 weight rows) x 64 (K) on v_mfma_f32_32x32x16_bf16
+// Two kernels, chosen per launch from the pair capacity: 256-row tiles where the MFMAs
+// bound the launch (below), and 128-row tiles where streaming the weights does:
+// tile 128 (M) x GM_BROWS (256 weight rows) x 64 (K) on v_mfma_f32_32x32x16_bf16
 // with fp32 accumulators: 4 compute waves in 2 x 2, each 64 x 128, plus 4 waves
 // that only issue the global->LDS copies (one of each kind per SIMD), so a wave
 // waiting for room in the memory queue never holds up the matrix cores.
@@ -518,11 +520,12 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
 // are skipped), instead of idling some SIMDs while the others run a full tile.  The K
 // loop is instantiated per count of active row blocks, so the common full tile runs
 // straight-line code with no per-block branches.  Every wave issues its share of the
-// next slice's global->LDS copies into the ring slot the previous step has just
-// released, one copy between every two MFMAs of the first two K sub-steps: issued all
-// at once after the barrier, the 64 copies of a step queue up in the texture path and
-// stall both waves of each SIMD until they drain.  The M tile is 256 rows, so per
-// expert the tiles are ceil(n_e / 256), counted in LDS at start.
+// global->LDS copies of the next input-row slice and of the weight slice two steps
+// ahead into the ring slots the previous step has just released, one copy between
+// every two MFMAs of the first two K sub-steps: issued all at once after the barrier,
+// the 64 copies of a step queue up in the texture path and stall both waves of each
+// SIMD until they drain.  The M tile is 256 rows, so per expert the tiles are
+// ceil(n_e / 256), counted at start.
 #ifndef RFX_TALL_MIN_ROWS
 #define RFX_TALL_MIN_ROWS 512
 #endif
