@@ -369,6 +369,54 @@ def test_grouped_swiglu(torch, name):
     assert np.isnan(oracle.bf16_to_f64(ybits[P:P + 256])).all()    # rows past P untouched
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_tall_swiglu_fuzz(torch, seed):
+    # The 256-row tile kernels (chosen where experts average 512 pair rows or more at
+    # capacity) on seeded random shapes: ragged and empty experts, expert sizes at tile
+    # edges, partial last N tiles (d % 256 = 128 in the down GEMM, f % 128 = 64 in the up
+    # GEMM), a single K step in the down GEMM (f = 64) and a gather with repeated tokens;
+    # every row of every expert against the fp64 definition, rows past P untouched.
+    from synth.workloads import bf16_bits_from_f32
+    L = _lib()
+    rng = np.random.default_rng([seed, 2608])
+    E = int(rng.choice([1, 2, 3, 5]))
+    d = int(rng.choice([128, 256, 384, 640]))
+    f = int(rng.choice([64, 128, 192, 320]))
+    T = int(rng.integers(64, 1200))
+    counts = rng.integers(0, 1300, E)
+    counts[rng.integers(0, E)] = rng.choice([0, 1, 255, 256, 257, 511, 512, 513])
+    P = int(counts.sum())
+    cap = max(P, 512 * E)
+    eo = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    st = np.zeros(cap, np.int32)
+    st[:P] = rng.integers(0, T, P)
+
+    def bf16(shape, scale):
+        return bf16_bits_from_f32((rng.standard_normal(shape) * scale).astype(np.float32))
+
+    h = bf16((T, d), 1.0)
+    wg, wu = bf16((E, f, d), d ** -0.5), bf16((E, f, d), d ** -0.5)
+    wd = bf16((E, d, f), 0.3 * f ** -0.5)
+    y = torch.full((cap, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(L.reflex_swiglu_workspace_size(cap, E, f), dtype=torch.uint8, device="cuda")
+    L.reflex_grouped_swiglu(to_device(h), to_device(st), to_device(eo), to_device(wg),
+                            to_device(wu), to_device(wd), y, ws)
+    torch.cuda.synchronize()
+    yb = bf16_bits(y)
+    got, ref = [], []
+    for e in range(E):
+        rows = np.arange(eo[e], eo[e + 1])
+        if len(rows):
+            x = oracle.bf16_to_f64(h[st[rows]])
+            ref.append(oracle.swiglu_expert(x, oracle.bf16_to_f64(wg[e]), oracle.bf16_to_f64(wu[e]),
+                                            oracle.bf16_to_f64(wd[e])))
+            got.append(oracle.bf16_to_f64(yb[rows]))
+    what = f"tall fuzz {seed}: E={E} T={T} d={d} f={f} counts={counts.tolist()}"
+    if got:
+        layer_tolerance_check(np.concatenate(got), np.concatenate(ref), what)
+    assert np.isnan(oracle.bf16_to_f64(yb[P:])).all(), what
+
+
 # --------------------------------------------------------------------------- combine
 @pytest.mark.parametrize("with_shared", [False, True])
 @pytest.mark.parametrize("T,d,E,kmax", [(1, 128, 4, 2), (333, 256, 16, 6), (1024, 2048, 64, 12),
