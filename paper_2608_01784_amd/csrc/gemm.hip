@@ -636,13 +636,16 @@ __global__ __launch_bounds__(TL_THREADS) void swiglu_gemm_tall_kernel(
     t.row_end = er1 < out_rows ? er1 : out_rows;
     if (t.row0 < 0 || t.row0 >= t.row_end) t.row_end = t.row0;   // inconsistent offsets: no rows
     // K rotation: tile (M tile m of its expert, N tile n) walks its K slices starting at
-    // slice n mod nk.  The tiles sharing an input-row slice (same m) then request it a
-    // step apart instead of all at once (5 % less GEMM time on the 16-layer stack, 3 %
-    // on the skewed layer, against no rotation), while the M tiles sharing a weight slice
-    // (same n) read it in the same step, so it comes from HBM once for all of them (1 %
-    // less time than a rotation of 2 m + n, which spread them two steps apart; traced in
-    // one process).  Only the order of the fp32 sums over K changes.
-    t.rot = (t.n0 / BN) % nk;
+    // slice n mod nk (down) or (n mod 2) mod nk (up).  The tiles sharing an input-row slice
+    // (same m) then request it a step apart instead of all at once (5 % less GEMM time on
+    // the 16-layer stack, 3 % on the skewed layer, against no rotation), while the M tiles
+    // sharing a weight slice (same n) read it in the same step, so it comes from HBM once
+    // for all of them (1 % less time than a rotation of 2 m + n, which spread them two
+    // steps apart).  In the up GEMM the 8 N tiles sharing a gathered-row slice stay within
+    // two steps, so fewer of its lines leave L2 before the last of them reads it (1 % less
+    // up-GEMM time than n mod nk; the same in the down GEMM made it 2-4 % slower).  All
+    // traced in one process.  Only the order of the fp32 sums over K changes.
+    t.rot = (UP ? (t.n0 / BN) % 2 : t.n0 / BN) % nk;
     return t;
   };
   const int total = m_total * n_tiles;
