@@ -368,15 +368,22 @@ __global__ __launch_bounds__(GM_THREADS) void swiglu_gemm_kernel(
     const uint16_t* a_ptr[GM_A_OPS];
     const uint16_t* b_ptr[GM_B_OPS];
     int ld_tile = -1;
-    // K rotation of the tile being loaded, (2 m + n) mod nk for M tile m of its expert
-    // and N tile n: the tiles sharing an input-row slice request it a step apart (as in
-    // the 256-row kernel below; 6 % less GEMM time on the LLaDA-MoE layer, measured)
+    // K rotation of the tile being loaded, (2 m + n + 5 e) mod nk for M tile m of expert
+    // e and N tile n (5 e in the up GEMM only): the tiles sharing an input-row slice
+    // request it a step apart (as in the 256-row kernel below; 6 % less GEMM time on the
+    // LLaDA-MoE layer, measured), and the tiles of different experts that stream weights
+    // at the same time start at different K slices.  With a weight row of 4 KB (d = 2048)
+    // and one M tile per expert, n alone gives the 256 concurrent tiles 8 distinct 128-byte
+    // offsets within their rows; spread over all 32, the LLaDA-MoE up GEMM took 103
+    // against 125 us (traced in one process, the same in three separate runs; the down
+    // GEMM, whose 2 KB rows already spread, was 1-2 % slower with it, 10 % slower with 8 e).
     int ld_rot = 0;
     auto setup_loader = [&](int tile_i) {
       const Tile t = decode_tile<GM_BM, BN>(l_begin + tile_i * per_xcd, s_tile_off, s_eo, E, dense_M,
                                      n_tiles, out_rows);
       const int rows_valid = t.row_end - t.row0;
-      ld_rot = (2 * ((t.row0 - (dense_M >= 0 ? 0 : s_eo[t.expert])) / GM_BM) + t.n0 / BN) % nk;
+      ld_rot = (2 * ((t.row0 - (dense_M >= 0 ? 0 : s_eo[t.expert])) / GM_BM) + t.n0 / BN +
+                (UP ? 5 * t.expert : 0)) % nk;
 #pragma unroll
       for (int j = 0; j < GM_A_OPS; ++j) {
         const int r = lane_row(GM_A_OPS * wv + j);
