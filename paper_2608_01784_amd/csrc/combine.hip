@@ -44,7 +44,11 @@ __device__ __forceinline__ uint4 load_row(const uint16_t* p) {
 // One token's output row (the body of the kernel below).  CB: expert rows in flight per
 // batch.  16 keep a token's rows in one batch on the small layers; from T = 4096 up, 8
 // (fewer registers, more workgroups resident per CU) are faster (16-layer stack layer:
-// 35.1 against 42.1 us; LLaDA-MoE layer: 7.4 against 7.1).
+// 35.1 against 42.1 us; LLaDA-MoE layer: 7.4 against 7.1).  A batch loads only the rows
+// the token has (the branch is uniform: one token per workgroup); loading the last row
+// again in the unused slots cost L2 requests for nothing (traced in one process: stack
+// layer with its residuals 52.6 -> 44.4 us, skewed layer 110.4 -> 105.3 us, LLaDA2.0-mini
+// 28.8 -> 27.0 us; batches of 2 or 4 rows with the extra loads were in between).
 template <int CB, bool STREAM>
 __device__ __forceinline__ void combine_token(
     int i, int p0, int p1, const uint16_t* __restrict__ y,
@@ -83,9 +87,12 @@ __device__ __forceinline__ void combine_token(
     for (int q = 0; q < (np > kWave ? 0 : np); q += CB) {
       uint4 r[CB];
 #pragma unroll
-      for (int u = 0; u < CB; ++u) {     // past the count: the last row again, not added
-        const int row = __builtin_amdgcn_readlane(prow, min(q + u, np - 1));
-        r[u] = load_row<STREAM>(y + static_cast<size_t>(row) * d + v);
+      for (int u = 0; u < CB; ++u) {
+        r[u] = zero;
+        if (q + u < np) {
+          const int row = __builtin_amdgcn_readlane(prow, q + u);
+          r[u] = load_row<STREAM>(y + static_cast<size_t>(row) * d + v);
+        }
       }
 #pragma unroll
       for (int u = 0; u < CB; ++u)
